@@ -1,0 +1,110 @@
+"""Plant plausible mistakes in the oracle (on the CPU, by monkeypatching) and
+check that at least one pin catches each of them."""
+import numpy as np
+import pytest
+
+from oracle import daso_oracle as O
+from tests import test_oracle_pins as pins
+
+F32 = np.float32
+
+
+def _merge_S_not_2S(xl, stale, S):
+    P = len(stale)
+    if P == 0:
+        return np.array(xl, dtype=np.float32, copy=True)
+    a = F32(S) * xl
+    for st in stale:
+        a = a + O.bf16_widen(st)
+    return a / F32(S + P)
+
+
+def _merge_wrong_denominator(xl, stale, S):
+    P = len(stale)
+    if P == 0:
+        return np.array(xl, dtype=np.float32, copy=True)
+    a = F32(2 * S) * xl
+    for st in stale:
+        a = a + O.bf16_widen(st)
+    return a / F32(2 * S + P + 1)
+
+
+def _merge_drops_last_copy(xl, stale, S):
+    P = len(stale)
+    if P == 0:
+        return np.array(xl, dtype=np.float32, copy=True)
+    a = F32(2 * S) * xl
+    for st in stale[:-1]:
+        a = a + O.bf16_widen(st)
+    return a / F32(2 * S + P)
+
+
+def _avg_drops_replica(grads):
+    s = np.array(grads[0], dtype=np.float32, copy=True)
+    for r in range(1, len(grads) - 1):
+        s = s + grads[r]
+    return s / F32(len(grads))
+
+
+def _avg_divides_by_g_minus_1(grads):
+    s = np.array(grads[0], dtype=np.float32, copy=True)
+    for r in range(1, len(grads)):
+        s = s + grads[r]
+    return s / F32(max(len(grads) - 1, 1))
+
+
+def _bf16_truncates(x):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    r = (x.view(np.uint32) >> 16).astype(np.uint16)
+    r[np.isnan(x)] = 0x7FC0
+    return r
+
+
+def _bf16_ties_away(x):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    r = ((u + np.uint64(0x8000)) >> np.uint64(16)).astype(np.uint16)
+    r[np.isnan(x)] = 0x7FC0
+    return r
+
+
+def _sgd_wrong_sign(x, m, gbar, lr, mu, wd):
+    m_new = (F32(mu) * m) + gbar
+    return x + (F32(lr) * m_new), m_new
+
+
+def _sgd_momentum_misplaced(x, m, gbar, lr, mu, wd):
+    m_new = F32(mu) * (m + gbar)
+    return x - (F32(lr) * m_new), m_new
+
+
+def _sgd_ignores_wd(x, m, gbar, lr, mu, wd):
+    m_new = (F32(mu) * m) + gbar
+    return x - (F32(lr) * m_new), m_new
+
+
+MUTANTS = [
+    ("merge_eq1", _merge_S_not_2S, [pins.test_merge_gradient_form_appendix,
+                                    pins.test_merge_small_integers_match_exact_rational_eq1]),
+    ("merge_eq1", _merge_wrong_denominator, [pins.test_merge_weights_sum_to_one,
+                                             pins.test_merge_gradient_form_appendix]),
+    ("merge_eq1", _merge_drops_last_copy, [pins.test_merge_zero_staleness_is_plain_mean_of_copies]),
+    ("local_avg", _avg_drops_replica, [pins.test_local_avg_matches_exact_rational_mean]),
+    ("local_avg", _avg_divides_by_g_minus_1, [pins.test_local_avg_close_to_fp64_mean]),
+    ("bf16_rne", _bf16_truncates, [pins.test_bf16_golden_encodings,
+                                   pins.test_bf16_rne_matches_bruteforce_every_high_half]),
+    ("bf16_rne", _bf16_ties_away, [pins.test_bf16_golden_encodings,
+                                   pins.test_bf16_rne_matches_torch_cast_on_finite_values]),
+    ("sgd_momentum", _sgd_wrong_sign, [pins.test_sgd_matches_torch_optim_sgd]),
+    ("sgd_momentum", _sgd_momentum_misplaced, [pins.test_sgd_matches_torch_optim_sgd]),
+    ("sgd_momentum", _sgd_ignores_wd, [pins.test_sgd_matches_torch_optim_sgd]),
+]
+
+
+@pytest.mark.parametrize("name,mutant,catchers", MUTANTS,
+                         ids=[m[1].__name__.lstrip("_") for m in MUTANTS])
+def test_pins_catch_planted_mistake(monkeypatch, name, mutant, catchers):
+    monkeypatch.setattr(O, name, mutant)
+    for pin in catchers:
+        with pytest.raises(AssertionError):
+            pin()
