@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Throughput of the fused DASO synchronisation step on one MI355X.
+
+One step = one daso_fused_sync_step over the whole parameter set of the
+workload (local gradient average over g replicas, SGD-momentum step, Eq. (1)
+merge of P bf16 copies per bucket, bf16 pack, per-bucket statistics), with all
+inputs resident in HBM.  Default workload: the ResNet-50-shaped parameter set
+(25,557,032 fp32 parameters in 161 tensors, 4 buckets of 25 MiB, g=4, P=8, S=4).
+
+Prints one JSON line (see the "metric"/"roofline"/"cpu_baseline" fields).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "fused_sync_resnet50_counters.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2104_05588_amd", "csrc", f)
+                  for f in ("daso_kernels.hip", "daso_launch.h")]
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source and this workload; else None."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    kv = {}
+    for ln in open(COUNTERS_FILE):
+        if ":" in ln and not ln.startswith("#"):
+            k, v = ln.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_source_sha() or kv.get("workload") != workload:
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, budget_s: float):
+    """The CPU oracle, as it is, on a bounded sample: the first bucket of the
+    workload, repeated until about `budget_s` seconds of oracle time."""
+    from oracle import daso_oracle as O
+    from workloads import generate as Gen
+
+    b = 0
+    part = Gen.host_bucket_inputs(w, b)
+    k = w.buckets[b].numel
+    bks = [(0, k, w.buckets[b].S)]
+    runs, spent = 0, 0.0
+    while spent < budget_s or runs == 0:
+        t0 = time.perf_counter()
+        O.fused_sync_step(part["grads"], part["params"], part["momentum"], part["stale"], bks,
+                          w.lr, w.mu, w.wd)
+        spent += time.perf_counter() - t0
+        runs += 1
+    return {"value": runs * k / spent, "unit": "params/s", "cores": 1, "kind": "oracle",
+            "sample": f"bucket 0 of {w.name} ({k} params, g={w.g}, P={w.P}, S={w.buckets[b].S}), "
+                      f"{runs} oracle steps in {spent:.1f} s; numpy ufuncs on one host thread "
+                      f"(host has {len(os.sched_getaffinity(0))} cores available)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="resnet50",
+                    choices=["tiny", "resnet18", "resnet50", "segnet", "gpt_medium"])
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run only a plain device copy of known size (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (the DASO sync step runs on one GPU's "
+              f"share with peer copies resident in HBM); --gpus {args.gpus} is not supported",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2104_05588_amd as daso
+    from workloads import generate as Gen
+    from workloads import recipes as R
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    daso.load()
+
+    if args.copy_probe:
+        nbytes = 1 << 30
+        src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": nbytes, "dispatches": args.steps}), flush=True)
+        return 0
+
+    w = R.workload(args.workload)
+    n = w.n
+    inp = Gen.device_inputs(w)
+    bks = [(b.start, b.numel, b.S) for b in w.buckets]
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    stats = daso.new_stats(len(bks))
+    step = daso.FusedStep(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                          w.lr, w.mu, w.wd, wire=wire, stats=stats)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
+    avg_ms = sum(kern_ms) / len(kern_ms)
+    med_ms = kern_ms[len(kern_ms) // 2]
+
+    # cold: evict the 256 MB Infinity Cache with a 1 GiB write before each timed call
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    cold = []
+    for i in range(min(args.steps, 20)):
+        scratch.fill_(float(i))
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        step()
+        e.record(stream)
+        e.synchronize()
+        cold.append(s.elapsed_time(e))
+    cold.sort()
+    del scratch
+
+    # plain device copy of the same footprint class, for context
+    cp_src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+    cp_dst = torch.empty_like(cp_src)
+    cp_dst.copy_(cp_src)
+    cs, ce = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cs.record(stream)
+    for _ in range(10):
+        cp_dst.copy_(cp_src)
+    ce.record(stream)
+    torch.cuda.synchronize()
+    copy_gbps = 10 * 2 * cp_src.numel() * 4 / (cs.elapsed_time(ce) * 1e-3) / 1e9
+    del cp_src, cp_dst
+
+    bpp = R.algorithmic_bytes_per_param(w.g, w.P)
+    alg_bytes = n * bpp
+    achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
+    traffic = counter_traffic(w.name)
+
+    out = {
+        "metric": "params synced/sec per fused DASO sync step (with achieved HBM GB/s as % of peak)",
+        "value": n * args.steps / wall,
+        "unit": "params/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 (bf16 wire and stale copies)",
+        "data": "synthetic: seeded device-generated params/grads/stale copies shaped like the network",
+        "config": {"workload": f"{w.name}-shaped fused DASO sync step", "params": n,
+                   "tensors": len(w.numels), "buckets": len(bks), "g": w.g, "P": w.P,
+                   "S": sorted({b.S for b in w.buckets}), "lr": w.lr, "mu": w.mu, "wd": w.wd,
+                   "wire": "bf16", "stats": True, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
+                     "kernel": "step_kernel<fused> (one launch per step)",
+                     "algorithmic_bytes_per_param": bpp, "algorithmic_bytes_per_launch": alg_bytes,
+                     "kernel_avg_us": avg_ms * 1e3, "kernel_median_us": med_ms * 1e3,
+                     "kernel_cold_median_us": cold[len(cold) // 2] * 1e3,
+                     "cold_frac": alg_bytes / (cold[len(cold) // 2] * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+                     "device_copy_GBps": copy_gbps},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,159 @@
+/*
+ * daso.h - C ABI of the DASO parameter-synchronisation step on MI355X (gfx950).
+ *
+ * DASO (Distributed Asynchronous and Selective Optimization, arXiv 2104.05588)
+ * synchronises data-parallel training in two levels.  Per GPU and per batch it
+ * averages the gradients of the g GPUs of its node (Section 3, Figure 2), takes a
+ * node-local optimizer step (Section 3.1; SGD with momentum in Section 4), and,
+ * when the exchange with the other nodes lands S batches late, merges the P
+ * received model states into the local one with the staleness-weighted average
+ * of Eq. (1):
+ *
+ *        x  <-  ( 2S * x_local + sum_{i=1..P} x_i ) / ( 2S + P )
+ *
+ * Parameters travel as bfloat16: they are cast while the send buffer is packed
+ * and cast back on receipt (Section 3; Section 4 names bfloat16).
+ *
+ * This library runs that per-element arithmetic for one GPU's parameters, held
+ * as flat buffers (all tensors of a model laid end to end) split into buckets,
+ * contiguous element ranges that each carry their own staleness S.
+ *
+ * Arithmetic contract.  Every floating-point operation is one IEEE-754 binary32
+ * operation rounded to nearest even, with no fused multiply-add, subnormals kept,
+ * correctly rounded division, in this order per element j:
+ *     s = G_0[j]; s = s + G_r[j] (r = 1..g-1);  gbar = s / g
+ *     d = gbar                 (weight_decay == 0)
+ *     d = gbar + weight_decay * x[j]     (otherwise)
+ *     m' = mu * m[j] + d ;  xl = x[j] - lr * m'
+ *     P == 0:  x' = xl
+ *     P >  0:  a = (2S) * xl ; a = a + widen(stale_i[j]) (i = 1..P) ; x' = a / (2S+P)
+ *     wire[j] = bf16_rne(x')   (or bf16_rne(xl) with DASO_PACK_PRE_MERGE)
+ * widen(h) places the bf16 pattern h in the top half of a binary32 (exact).
+ * bf16_rne rounds to nearest with ties to even; +-inf stay infinite, finite
+ * values past the largest bfloat16 round to infinity, NaN becomes 0x7FC0.
+ * Results are deterministic: the same inputs give the same bits on every call.
+ *
+ * Conventions for every entry point.
+ *  - Buffers are device memory owned by the caller (the library allocates none of
+ *    them).  fp32 buffers hold n floats, bf16 buffers hold n uint16 bit patterns.
+ *  - Every device base pointer must be 16-byte aligned (DASO_EALIGN otherwise).
+ *  - Host pointer arrays (grads, stale) and bucket tables are read during the call
+ *    only; the caller may free or reuse them as soon as the call returns.
+ *  - Work is enqueued on `stream` (0 = the null stream) and runs asynchronously;
+ *    no call synchronises the device or the stream.
+ *  - n == 0 is a valid no-op.
+ *  - On any error nothing is launched and a negative status is returned; the
+ *    buffers are untouched.  daso_status_string names the status.
+ *  - Calls may be made from several host threads.  Fused steps with statistics
+ *    share one small per-(device, stream) workspace that the library allocates on
+ *    first use and keeps until the process ends; calls on one stream are ordered
+ *    by that stream.
+ */
+#ifndef DASO_H
+#define DASO_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define DASO_OK 0
+#define DASO_EINVAL (-1)  /* null required pointer, bad count, S < 0, buckets not a tiling of [0,n) */
+#define DASO_EALIGN (-2)  /* a device base pointer is not 16-byte aligned */
+#define DASO_EALIAS (-3)  /* an output overlaps an input other than in the allowed in-place pairs */
+#define DASO_EHIP (-4)    /* a HIP call (launch, allocation of the stats workspace) failed */
+
+#define DASO_MAX_G 64     /* most replica gradients per call */
+#define DASO_MAX_P 64     /* most exchanged copies per call */
+
+/* flags of daso_sync_args */
+#define DASO_PACK_PRE_MERGE 1u /* pack xl (after the optimizer step, before Eq. (1)) instead of x' */
+
+/* A bucket: elements [start, start + numel) merged with staleness S (S >= 0).
+ * S is the number of batches the exchanged copies are late (Eq. (1)); S = 0
+ * gives the plain average of the copies, as in blocking synchronisation. */
+typedef struct daso_bucket {
+  int64_t start;
+  int64_t numel;
+  int32_t S;
+  int32_t reserved; /* must be 0 */
+} daso_bucket;
+
+/* Per-bucket side outputs of a fused step (not part of the paper's method):
+ * grad_sq = sum of gbar^2, delta_sq = sum of (x' - xl)^2, both accumulated in
+ * binary64 from the binary32 values; nonfinite = number of elements whose x' is
+ * NaN or infinite.  The summation order is fixed, so the values are deterministic
+ * but may differ from another order in the last bits. */
+typedef struct daso_bucket_stats {
+  double grad_sq;
+  double delta_sq;
+  uint64_t nonfinite;
+} daso_bucket_stats;
+
+/* Arguments of daso_fused_sync_step. */
+typedef struct daso_sync_args {
+  int64_t n;                       /* parameters on this GPU */
+  int32_t g;                       /* replica gradients, 1..DASO_MAX_G */
+  int32_t P;                       /* exchanged copies, 0..DASO_MAX_P */
+  const float* const* grads;       /* host array of g device pointers, each n fp32; read only */
+  const uint16_t* const* stale;    /* host array of P device pointers, each n bf16; read only
+                                      (may be NULL when P == 0) */
+  float* params;                   /* n fp32, read and overwritten with x' */
+  float* momentum;                 /* n fp32, read and overwritten with m' */
+  uint16_t* wire;                  /* n bf16 written, or NULL for no packing */
+  float* grad_avg;                 /* n fp32 written with gbar, or NULL; may be exactly
+                                      one of the grads buffers (Figure 2: every replica's
+                                      gradients become the average) */
+  const daso_bucket* buckets;      /* host array; the buckets must tile [0, n) */
+  int32_t nbuckets;                /* >= 1 when n > 0 */
+  float lr;                        /* learning rate */
+  float mu;                        /* momentum factor */
+  float weight_decay;              /* coupled L2 term; 0 skips it */
+  uint32_t flags;                  /* DASO_PACK_PRE_MERGE or 0 */
+  daso_bucket_stats* stats;        /* device array of nbuckets entries written, or NULL */
+} daso_sync_args;
+
+/* Local synchronisation (Section 3, Figure 2): out[j] = (sum_r grads[r][j]) / g,
+ * summed in replica order.  grads: host array of g (1..DASO_MAX_G) device pointers
+ * to n fp32 each.  out: n fp32; it may be exactly one of the grads buffers but
+ * must not otherwise overlap them.  Reads 4g bytes and writes 4 bytes per element. */
+int daso_local_avg(const float* const* grads, int32_t g, float* out, int64_t n,
+                   hipStream_t stream);
+
+/* Buffer packaging for the global exchange (Section 3; bfloat16 per Section 4):
+ * wire[j] = bf16_rne(src[j]).  src: n fp32; wire: n uint16, must not overlap src. */
+int daso_pack_bf16(const float* src, uint16_t* wire, int64_t n, hipStream_t stream);
+
+/* Eq. (1), in place, bucket by bucket: params[j] <- (2S*params[j] + sum_i
+ * widen(stale[i][j])) / (2S + P) with the S of the bucket holding j; P == 0
+ * leaves params unchanged.  stale: host array of P (0..DASO_MAX_P) device
+ * pointers to n bf16 each, none overlapping params.  buckets: host array of
+ * nbuckets entries tiling [0, n).  wire: NULL, or n uint16 receiving
+ * bf16_rne of the merged parameters (must not overlap any other buffer). */
+int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P,
+                      const daso_bucket* buckets, int32_t nbuckets, uint16_t* wire,
+                      int64_t n, hipStream_t stream);
+
+/* One DASO synchronisation step for one GPU's parameters, in a single pass over
+ * memory: local gradient average, SGD-momentum step, Eq. (1) merge per bucket,
+ * bf16 pack and (optionally) the per-bucket statistics.  Aliasing rules: params
+ * and momentum are updated in place and must not overlap each other or any other
+ * buffer; wire, stats and grad_avg (apart from the allowed grads alias) must not
+ * overlap anything else; inputs may overlap each other. */
+int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* daso_status_string(int status);
+
+/* ABI version of this header (major * 100 + minor). */
+int daso_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DASO_H */

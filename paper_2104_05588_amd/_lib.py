@@ -1,0 +1,222 @@
+"""Thin ctypes binding of libdaso.so (declared in include/daso.h).
+
+Argument marshalling only: tensors are checked for device, dtype, size and
+contiguity, their device addresses and the current HIP stream cross the C ABI,
+and every step of the computation runs in the library's kernels.  There is no
+fallback: if the library is not built, or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdaso.so")
+
+DASO_OK = 0
+DASO_EINVAL = -1
+DASO_EALIGN = -2
+DASO_EALIAS = -3
+DASO_EHIP = -4
+DASO_MAX_G = 64
+DASO_MAX_P = 64
+DASO_PACK_PRE_MERGE = 1
+
+EXPORTED = ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_fused_sync_step",
+            "daso_status_string", "daso_abi_version")
+
+
+class daso_bucket(ctypes.Structure):
+    _fields_ = [("start", ctypes.c_int64), ("numel", ctypes.c_int64),
+                ("S", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class daso_bucket_stats(ctypes.Structure):
+    _fields_ = [("grad_sq", ctypes.c_double), ("delta_sq", ctypes.c_double),
+                ("nonfinite", ctypes.c_uint64)]
+
+
+class daso_sync_args(ctypes.Structure):
+    _fields_ = [
+        ("n", ctypes.c_int64), ("g", ctypes.c_int32), ("P", ctypes.c_int32),
+        ("grads", ctypes.POINTER(ctypes.c_void_p)), ("stale", ctypes.POINTER(ctypes.c_void_p)),
+        ("params", ctypes.c_void_p), ("momentum", ctypes.c_void_p),
+        ("wire", ctypes.c_void_p), ("grad_avg", ctypes.c_void_p),
+        ("buckets", ctypes.POINTER(daso_bucket)), ("nbuckets", ctypes.c_int32),
+        ("lr", ctypes.c_float), ("mu", ctypes.c_float), ("weight_decay", ctypes.c_float),
+        ("flags", ctypes.c_uint32), ("stats", ctypes.c_void_p),
+    ]
+
+
+class DasoError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libdaso.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2104_05588_amd.build` "
+                           "(there is no fallback implementation)")
+    # torch is imported first so that its HIP runtime is the one the library binds to
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.daso_local_avg.argtypes = [ctypes.POINTER(vp), i32, vp, i64, vp]
+    lib.daso_pack_bf16.argtypes = [vp, vp, i64, vp]
+    lib.daso_global_merge.argtypes = [vp, ctypes.POINTER(vp), i32, ctypes.POINTER(daso_bucket), i32,
+                                      vp, i64, vp]
+    lib.daso_fused_sync_step.argtypes = [ctypes.POINTER(daso_sync_args), vp]
+    lib.daso_status_string.argtypes = [ctypes.c_int]
+    lib.daso_status_string.restype = ctypes.c_char_p
+    lib.daso_abi_version.argtypes = []
+    for name in ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_fused_sync_step",
+                 "daso_abi_version"):
+        getattr(lib, name).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().daso_status_string(int(status)).decode()
+
+
+# ------------------------------------------------------------- marshalling
+def _stream_handle(stream: Optional[torch.cuda.Stream]) -> ctypes.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor], dtypes: Tuple[torch.dtype, ...], n: int, what: str) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{what} must have dtype in {dtypes}, got {t.dtype}")
+    if t.numel() != n or not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous with {n} elements")
+    return t.data_ptr()
+
+
+_F32 = (torch.float32,)
+_BF16 = (torch.int16, torch.bfloat16, torch.uint16)
+
+
+def _ptr_array(ts: Sequence[torch.Tensor], dtypes, n: int, what: str):
+    arr = (ctypes.c_void_p * max(len(ts), 1))()
+    for i, t in enumerate(ts):
+        arr[i] = _ptr(t, dtypes, n, f"{what}[{i}]")
+    return arr
+
+
+def bucket_table(buckets: Sequence[Tuple[int, int, int]]):
+    arr = (daso_bucket * max(len(buckets), 1))()
+    for i, (s, k, S) in enumerate(buckets):
+        arr[i].start, arr[i].numel, arr[i].S, arr[i].reserved = int(s), int(k), int(S), 0
+    return arr
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != DASO_OK:
+        raise DasoError(rc, what)
+
+
+# --------------------------------------------------------------- the calls
+def local_avg(grads: Sequence[torch.Tensor], out: torch.Tensor, stream=None) -> torch.Tensor:
+    """out = mean of the replica gradients (local synchronisation)."""
+    n = out.numel()
+    arr = _ptr_array(grads, _F32, n, "grads")
+    _check(load().daso_local_avg(arr, len(grads), _ptr(out, _F32, n, "out"), n, _stream_handle(stream)),
+           "daso_local_avg")
+    return out
+
+
+def pack_bf16(src: torch.Tensor, wire: torch.Tensor, stream=None) -> torch.Tensor:
+    """wire = bf16 round-to-nearest-even bit patterns of src."""
+    n = src.numel()
+    _check(load().daso_pack_bf16(_ptr(src, _F32, n, "src"), _ptr(wire, _BF16, n, "wire"), n,
+                                 _stream_handle(stream)), "daso_pack_bf16")
+    return wire
+
+
+def global_merge(params: torch.Tensor, stale: Sequence[torch.Tensor],
+                 buckets: Sequence[Tuple[int, int, int]], wire: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    """Eq. (1) merge of the exchanged bf16 copies into params, in place."""
+    n = params.numel()
+    arr = _ptr_array(stale, _BF16, n, "stale")
+    bt = bucket_table(buckets)
+    _check(load().daso_global_merge(_ptr(params, _F32, n, "params"), arr, len(stale), bt, len(buckets),
+                                    _ptr(wire, _BF16, n, "wire"), n, _stream_handle(stream)),
+           "daso_global_merge")
+    return params
+
+
+def new_stats(nbuckets: int, device="cuda") -> torch.Tensor:
+    """Device buffer for per-bucket statistics: float64 [nbuckets, 3] whose third
+    column holds the uint64 non-finite count (read it with decode_stats)."""
+    return torch.zeros((nbuckets, 3), dtype=torch.float64, device=device)
+
+
+def decode_stats(stats: torch.Tensor) -> List[Tuple[float, float, int]]:
+    h = stats.detach().cpu()
+    counts = h[:, 2].contiguous().view(torch.int64)
+    return [(float(h[i, 0]), float(h[i, 1]), int(counts[i])) for i in range(h.shape[0])]
+
+
+class FusedStep:
+    """A prepared daso_fused_sync_step: argument checks and marshalling happen
+    once here, so that each call costs one C call.  The tensors must stay alive
+    (and keep their storage) while the object is used."""
+
+    def __init__(self, grads: Sequence[torch.Tensor], params: torch.Tensor, momentum: torch.Tensor,
+                 stale: Sequence[torch.Tensor], buckets: Sequence[Tuple[int, int, int]],
+                 lr: float, mu: float, weight_decay: float = 0.0, wire: Optional[torch.Tensor] = None,
+                 grad_avg: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None,
+                 flags: int = 0):
+        n = params.numel()
+        self._keep = (list(grads), params, momentum, list(stale), wire, grad_avg, stats)
+        self._grads = _ptr_array(grads, _F32, n, "grads")
+        self._stale = _ptr_array(stale, _BF16, n, "stale")
+        self._buckets = bucket_table(buckets)
+        if stats is not None:
+            if not stats.is_cuda or stats.dtype != torch.float64 or tuple(stats.shape) != (len(buckets), 3) \
+                    or not stats.is_contiguous():
+                raise ValueError("stats must be a contiguous float64 device tensor of shape [nbuckets, 3]")
+        a = daso_sync_args()
+        a.n, a.g, a.P = n, len(grads), len(stale)
+        a.grads = self._grads
+        a.stale = self._stale
+        a.params = _ptr(params, _F32, n, "params")
+        a.momentum = _ptr(momentum, _F32, n, "momentum")
+        a.wire = _ptr(wire, _BF16, n, "wire")
+        a.grad_avg = _ptr(grad_avg, _F32, n, "grad_avg")
+        a.buckets = self._buckets
+        a.nbuckets = len(buckets)
+        a.lr, a.mu, a.weight_decay = float(lr), float(mu), float(weight_decay)
+        a.flags = int(flags)
+        a.stats = stats.data_ptr() if stats is not None else None
+        self.args = a
+        self._byref = ctypes.byref(a)
+        self._fn = load().daso_fused_sync_step
+
+    def __call__(self, stream=None) -> None:
+        _check(self._fn(self._byref, _stream_handle(stream)), "daso_fused_sync_step")
+
+
+def fused_sync_step(grads, params, momentum, stale, buckets, lr, mu, weight_decay=0.0, wire=None,
+                    grad_avg=None, stats=None, flags=0, stream=None) -> None:
+    """One DASO synchronisation step (see include/daso.h), in place on params
+    and momentum; writes wire, grad_avg and stats when given."""
+    FusedStep(grads, params, momentum, stale, buckets, lr, mu, weight_decay, wire, grad_avg, stats,
+              flags)(stream)

@@ -1,0 +1,302 @@
+// C-ABI entry points of the DASO synchronisation library: argument checks,
+// bucket tables, the per-stream statistics workspace, and launches.
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <utility>
+#include <vector>
+
+#include "daso_launch.h"
+
+namespace {
+
+using daso::StepArgs;
+using daso::TileBucket;
+using daso::TilePartial;
+
+constexpr int32_t kMaxS = 1 << 20;  // 2S and 2S + P stay exact in binary32
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Span {
+  uintptr_t lo, hi;  // [lo, hi) in bytes
+};
+
+Span span_of(const void* p, int64_t n, size_t esz) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return {lo, lo + static_cast<uintptr_t>(n) * esz};
+}
+
+bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Buckets must tile [0, n): sorted by start they are back to back.
+int check_buckets(const daso_bucket* b, int32_t nb, int64_t n) {
+  if (nb < 1 || b == nullptr) return DASO_EINVAL;
+  std::vector<std::pair<int64_t, int64_t>> s;
+  s.reserve(static_cast<size_t>(nb));
+  for (int32_t i = 0; i < nb; ++i) {
+    if (b[i].numel < 0 || b[i].start < 0 || b[i].S < 0 || b[i].S > kMaxS || b[i].reserved != 0)
+      return DASO_EINVAL;
+    s.emplace_back(b[i].start, b[i].numel);
+  }
+  std::sort(s.begin(), s.end());
+  int64_t pos = 0;
+  for (const auto& e : s) {
+    if (e.first != pos) return DASO_EINVAL;
+    pos += e.second;
+  }
+  return pos == n ? DASO_OK : DASO_EINVAL;
+}
+
+// ---------------------------------------------------------------- workspace
+// Per (device, stream): a 256-byte counter slot followed by per-tile partials.
+// Allocated on first use and grown when a larger launch needs it; the counter
+// is zeroed once at allocation and the kernel leaves it at zero.
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+int workspace_for(hipStream_t stream, size_t need, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return DASO_EHIP;
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  Workspace& w = g_ws[{dev, stream}];
+  if (w.bytes < need) {
+    if (w.ptr) {
+      // earlier launches on this stream may still read the old buffer
+      if (hipStreamSynchronize(stream) != hipSuccess) return DASO_EHIP;
+      (void)hipFree(w.ptr);
+      w.ptr = nullptr;
+      w.bytes = 0;
+    }
+    size_t bytes = std::max<size_t>(need, size_t(1) << 20);
+    if (hipMalloc(&w.ptr, bytes) != hipSuccess) {
+      w.ptr = nullptr;
+      return DASO_EHIP;
+    }
+    if (hipMemsetAsync(w.ptr, 0, bytes, stream) != hipSuccess) return DASO_EHIP;
+    w.bytes = bytes;
+  }
+  *out = w.ptr;
+  return DASO_OK;
+}
+
+// -------------------------------------------------------------- launching
+struct Group {
+  int32_t first;  // index of its first bucket in the caller's table
+  int32_t count;
+  int64_t ntiles;
+};
+
+// Cut the caller's bucket table into launches of at most kLaunchBuckets buckets.
+std::vector<Group> group_buckets(const daso_bucket* b, int32_t nb) {
+  std::vector<Group> out;
+  for (int32_t i = 0; i < nb; i += daso::kLaunchBuckets) {
+    Group gr{i, std::min<int32_t>(daso::kLaunchBuckets, nb - i), 0};
+    for (int32_t k = 0; k < gr.count; ++k)
+      gr.ntiles += daso::tiles_of(b[i + k].start, b[i + k].start + b[i + k].numel);
+    out.push_back(gr);
+  }
+  return out;
+}
+
+void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr) {
+  int64_t t = 0;
+  for (int32_t k = 0; k < gr.count; ++k) {
+    const daso_bucket& s = b[gr.first + k];
+    a.b[k].start = s.start;
+    a.b[k].end = s.start + s.numel;
+    a.b[k].first_tile = static_cast<int32_t>(t);
+    a.b[k].S = s.S;
+    t += daso::tiles_of(s.start, s.start + s.numel);
+  }
+  a.nb = gr.count;
+  // A launch needs at least one workgroup, even over empty buckets, so that
+  // their statistics are still written (as zeros).
+  a.ntiles = static_cast<int32_t>(std::max<int64_t>(t, 1));
+}
+
+int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
+               daso_bucket_stats* stats, hipStream_t stream) {
+  const std::vector<Group> groups = group_buckets(b, nb);
+  int64_t max_tiles = 1;
+  for (const auto& gr : groups) {
+    if (gr.ntiles > INT32_MAX) return DASO_EINVAL;
+    max_tiles = std::max(max_tiles, gr.ntiles);
+  }
+  const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
+  if (with_stats) {
+    void* ws = nullptr;
+    const int rc = workspace_for(stream, 256 + static_cast<size_t>(max_tiles) * sizeof(TilePartial), &ws);
+    if (rc != DASO_OK) return rc;
+    a.counter = static_cast<unsigned int*>(ws);
+    a.partials = reinterpret_cast<TilePartial*>(static_cast<char*>(ws) + 256);
+  }
+  for (const auto& gr : groups) {
+    fill_group(a, b, gr);
+    a.stats = with_stats ? stats + gr.first : nullptr;
+    if (daso::launch_step(mode, with_stats, a, stream) != hipSuccess) return DASO_EHIP;
+  }
+  return DASO_OK;
+}
+
+int check_ptr_table(const void* const* p, int32_t count) {
+  if (count > 0 && p == nullptr) return DASO_EINVAL;
+  for (int32_t i = 0; i < count; ++i) {
+    if (p[i] == nullptr) return DASO_EINVAL;
+    if (!aligned16(p[i])) return DASO_EALIGN;
+  }
+  return DASO_OK;
+}
+
+int check_out(const void* p) {
+  if (p == nullptr) return DASO_EINVAL;
+  return aligned16(p) ? DASO_OK : DASO_EALIGN;
+}
+
+}  // namespace
+
+extern "C" {
+
+int daso_abi_version(void) { return 100; }
+
+const char* daso_status_string(int status) {
+  switch (status) {
+    case DASO_OK: return "DASO_OK: success";
+    case DASO_EINVAL: return "DASO_EINVAL: invalid argument (null pointer, count out of range, S < 0, or buckets not tiling [0, n))";
+    case DASO_EALIGN: return "DASO_EALIGN: a device buffer is not 16-byte aligned";
+    case DASO_EALIAS: return "DASO_EALIAS: an output buffer overlaps another buffer";
+    case DASO_EHIP: return "DASO_EHIP: a HIP call failed";
+    default: return "unknown DASO status";
+  }
+}
+
+int daso_local_avg(const float* const* grads, int32_t g, float* out, int64_t n, hipStream_t stream) {
+  if (n < 0 || g < 1 || g > DASO_MAX_G) return DASO_EINVAL;
+  int rc = check_ptr_table(reinterpret_cast<const void* const*>(grads), g);
+  if (rc != DASO_OK) return rc;
+  if ((rc = check_out(out)) != DASO_OK) return rc;
+  const Span so = span_of(out, n, 4);
+  for (int32_t r = 0; r < g; ++r)
+    if (grads[r] != out && overlaps(so, span_of(grads[r], n, 4))) return DASO_EALIAS;
+  if (n == 0) return DASO_OK;
+
+  StepArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int32_t r = 0; r < g; ++r) a.grads[r] = grads[r];
+  a.g = g;
+  a.gavg = out;
+  const daso_bucket whole = {0, n, 0, 0};
+  return run_groups(daso::kModeAvg, a, &whole, 1, nullptr, stream);
+}
+
+int daso_pack_bf16(const float* src, uint16_t* wire, int64_t n, hipStream_t stream) {
+  if (n < 0) return DASO_EINVAL;
+  int rc = check_out(src);
+  if (rc != DASO_OK) return rc;
+  if ((rc = check_out(wire)) != DASO_OK) return rc;
+  if (overlaps(span_of(src, n, 4), span_of(wire, n, 2))) return DASO_EALIAS;
+  if (n == 0) return DASO_OK;
+
+  StepArgs a;
+  memset(&a, 0, sizeof(a));
+  a.src = src;
+  a.wire = wire;
+  const daso_bucket whole = {0, n, 0, 0};
+  return run_groups(daso::kModePack, a, &whole, 1, nullptr, stream);
+}
+
+int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P, const daso_bucket* buckets,
+                      int32_t nbuckets, uint16_t* wire, int64_t n, hipStream_t stream) {
+  if (n < 0 || P < 0 || P > DASO_MAX_P) return DASO_EINVAL;
+  int rc = check_out(params);
+  if (rc != DASO_OK) return rc;
+  if ((rc = check_ptr_table(reinterpret_cast<const void* const*>(stale), P)) != DASO_OK) return rc;
+  if (wire && !aligned16(wire)) return DASO_EALIGN;
+  if (n == 0) return DASO_OK;
+  if ((rc = check_buckets(buckets, nbuckets, n)) != DASO_OK) return rc;
+  const Span sx = span_of(params, n, 4);
+  for (int32_t i = 0; i < P; ++i)
+    if (overlaps(sx, span_of(stale[i], n, 2))) return DASO_EALIAS;
+  if (wire) {
+    const Span sw = span_of(wire, n, 2);
+    if (overlaps(sw, sx)) return DASO_EALIAS;
+    for (int32_t i = 0; i < P; ++i)
+      if (overlaps(sw, span_of(stale[i], n, 2))) return DASO_EALIAS;
+  }
+
+  StepArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int32_t i = 0; i < P; ++i) a.stale[i] = stale[i];
+  a.P = P;
+  a.x = params;
+  a.wire = wire;
+  return run_groups(daso::kModeMerge, a, buckets, nbuckets, nullptr, stream);
+}
+
+int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
+  if (args == nullptr) return DASO_EINVAL;
+  const daso_sync_args& s = *args;
+  if (s.n < 0 || s.g < 1 || s.g > DASO_MAX_G || s.P < 0 || s.P > DASO_MAX_P) return DASO_EINVAL;
+  int rc = check_ptr_table(reinterpret_cast<const void* const*>(s.grads), s.g);
+  if (rc != DASO_OK) return rc;
+  if ((rc = check_ptr_table(reinterpret_cast<const void* const*>(s.stale), s.P)) != DASO_OK) return rc;
+  if ((rc = check_out(s.params)) != DASO_OK) return rc;
+  if ((rc = check_out(s.momentum)) != DASO_OK) return rc;
+  if (s.wire && !aligned16(s.wire)) return DASO_EALIGN;
+  if (s.grad_avg && !aligned16(s.grad_avg)) return DASO_EALIGN;
+  if (s.stats && (reinterpret_cast<uintptr_t>(s.stats) & 7u) != 0) return DASO_EALIGN;
+  if ((s.flags & ~DASO_PACK_PRE_MERGE) != 0) return DASO_EINVAL;
+  if (s.n == 0) return DASO_OK;
+  if ((rc = check_buckets(s.buckets, s.nbuckets, s.n)) != DASO_OK) return rc;
+
+  // outputs: params and momentum (in place), wire, grad_avg, stats
+  const Span sx = span_of(s.params, s.n, 4);
+  const Span sm = span_of(s.momentum, s.n, 4);
+  std::vector<Span> inputs;
+  for (int32_t r = 0; r < s.g; ++r) inputs.push_back(span_of(s.grads[r], s.n, 4));
+  for (int32_t i = 0; i < s.P; ++i) inputs.push_back(span_of(s.stale[i], s.n, 2));
+  std::vector<Span> outs = {sx, sm};
+  if (s.wire) outs.push_back(span_of(s.wire, s.n, 2));
+  if (s.stats) outs.push_back(span_of(s.stats, s.nbuckets, sizeof(daso_bucket_stats)));
+  for (size_t i = 0; i < outs.size(); ++i) {
+    for (size_t j = i + 1; j < outs.size(); ++j)
+      if (overlaps(outs[i], outs[j])) return DASO_EALIAS;
+    for (const Span& in : inputs)
+      if (overlaps(outs[i], in)) return DASO_EALIAS;
+  }
+  if (s.grad_avg) {
+    const Span sg = span_of(s.grad_avg, s.n, 4);
+    for (const Span& o : outs)
+      if (overlaps(sg, o)) return DASO_EALIAS;
+    for (int32_t i = 0; i < s.P; ++i)
+      if (overlaps(sg, inputs[static_cast<size_t>(s.g + i)])) return DASO_EALIAS;
+    for (int32_t r = 0; r < s.g; ++r)
+      if (s.grads[r] != s.grad_avg && overlaps(sg, inputs[static_cast<size_t>(r)])) return DASO_EALIAS;
+  }
+
+  StepArgs a;
+  memset(&a, 0, sizeof(a));
+  for (int32_t r = 0; r < s.g; ++r) a.grads[r] = s.grads[r];
+  for (int32_t i = 0; i < s.P; ++i) a.stale[i] = s.stale[i];
+  a.g = s.g;
+  a.P = s.P;
+  a.x = s.params;
+  a.m = s.momentum;
+  a.wire = s.wire;
+  a.gavg = s.grad_avg;
+  a.lr = s.lr;
+  a.mu = s.mu;
+  a.wd = s.weight_decay;
+  a.flags = s.flags;
+  return run_groups(daso::kModeFused, a, s.buckets, s.nbuckets, s.stats, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,351 @@
+// HIP kernels of the DASO synchronisation step for CDNA4 (gfx950).
+//
+// The step is a pure streaming computation: every output element depends only
+// on the same element of each input stream, so the kernels read each stream
+// once with 16-byte (fp32) or 8-byte (bf16) coalesced loads, keep everything
+// in registers, and write each output once.  It is bound by HBM bandwidth, not
+// arithmetic; there is no contraction, so no MFMA.
+//
+// Arithmetic follows the binary32 operation order stated in daso.h exactly
+// (local average: Section 3, Figure 2; optimizer step: Sections 3.1 and 4;
+// merge: Eq. (1); bf16 packing: Sections 3 and 4).  Floating-point contraction
+// is off for this file and division is the correctly rounded one, so the
+// results match a plain IEEE binary32 evaluation bit for bit.
+#include "daso_launch.h"
+
+#pragma clang fp contract(off)
+
+namespace daso {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// ------------------------------------------------------------ memory helpers
+// FULL: the 4-element vector lies inside the tile; otherwise `mask` selects
+// the elements to touch (bit k = element e0 + k) and the rest read as 0.
+template <bool FULL, bool STREAM>
+__device__ __forceinline__ f32x4 load_f32(const float* __restrict__ p, int64_t e0, unsigned mask) {
+  if constexpr (FULL) {
+    const f32x4* v = reinterpret_cast<const f32x4*>(p + e0);
+    if constexpr (STREAM) return __builtin_nontemporal_load(v);
+    else return *v;
+  } else {
+    f32x4 r = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (mask & (1u << k)) r[k] = p[e0 + k];
+    return r;
+  }
+}
+
+template <bool FULL>
+__device__ __forceinline__ u32x2 load_bf16(const uint16_t* __restrict__ p, int64_t e0, unsigned mask) {
+  if constexpr (FULL) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p + e0));
+  } else {
+    uint32_t h[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (mask & (1u << k)) h[k] = p[e0 + k];
+    u32x2 r;
+    r.x = h[0] | (h[1] << 16);
+    r.y = h[2] | (h[3] << 16);
+    return r;
+  }
+}
+
+template <bool FULL, bool STREAM>
+__device__ __forceinline__ void store_f32(float* __restrict__ p, int64_t e0, unsigned mask, f32x4 v) {
+  if constexpr (FULL) {
+    f32x4* d = reinterpret_cast<f32x4*>(p + e0);
+    if constexpr (STREAM) __builtin_nontemporal_store(v, d);
+    else *d = v;
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (mask & (1u << k)) p[e0 + k] = v[k];
+  }
+}
+
+template <bool FULL>
+__device__ __forceinline__ void store_bf16(uint16_t* __restrict__ p, int64_t e0, unsigned mask, u32x2 w) {
+  if constexpr (FULL) {
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(p + e0));
+  } else {
+    const uint32_t h[4] = {w.x & 0xFFFFu, w.x >> 16, w.y & 0xFFFFu, w.y >> 16};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (mask & (1u << k)) p[e0 + k] = static_cast<uint16_t>(h[k]);
+  }
+}
+
+// ------------------------------------------------------------ bf16 helpers
+// binary32 -> bfloat16, round to nearest even: add 0x7FFF plus the lowest kept
+// bit and drop the low half; a mantissa carry moves to the next binade or to
+// infinity.  NaN becomes the quiet NaN 0x7FC0.
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  return ((u & 0x7FFFFFFFu) > 0x7F800000u) ? 0x7FC0u : r;
+}
+
+__device__ __forceinline__ u32x2 pack4(f32x4 v) {
+  u32x2 w;
+  w.x = bf16_rne(v.x) | (bf16_rne(v.y) << 16);
+  w.y = bf16_rne(v.z) | (bf16_rne(v.w) << 16);
+  return w;
+}
+
+// Exact bfloat16 -> binary32: the pattern becomes the top half.
+__device__ __forceinline__ f32x4 widen4(u32x2 h) {
+  f32x4 r;
+  r.x = __uint_as_float(h.x << 16);
+  r.y = __uint_as_float(h.x & 0xFFFF0000u);
+  r.z = __uint_as_float(h.y << 16);
+  r.w = __uint_as_float(h.y & 0xFFFF0000u);
+  return r;
+}
+
+// Division by a per-bucket or per-call constant.  For a power of two the
+// product with its (exact) reciprocal equals the correctly rounded quotient.
+struct Divisor {
+  float d;
+  float inv;
+  bool pow2;
+};
+
+__device__ __forceinline__ Divisor make_divisor(int k) {
+  Divisor v;
+  v.d = static_cast<float>(k);
+  v.pow2 = k > 0 && (k & (k - 1)) == 0;
+  v.inv = v.pow2 ? 1.0f / v.d : 0.0f;
+  return v;
+}
+
+__device__ __forceinline__ f32x4 divide(f32x4 a, const Divisor& q) {
+  if (q.pow2) return a * q.inv;
+  f32x4 r;
+  r.x = a.x / q.d;
+  r.y = a.y / q.d;
+  r.z = a.z / q.d;
+  r.w = a.w / q.d;
+  return r;
+}
+
+// --------------------------------------------------------------- statistics
+// Per-thread sums over a tile (the count fits 32 bits: at most 32 elements per
+// thread); the cross-tile reduction uses a 64-bit count.
+template <typename CountT>
+struct AccT {
+  double gsq;
+  double dsq;
+  CountT nf;
+};
+using Acc = AccT<uint32_t>;
+using Acc64 = AccT<uint64_t>;
+
+__device__ __forceinline__ void accumulate(Acc& acc, f32x4 gbar, f32x4 xl, f32x4 xn, unsigned mask) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (mask & (1u << k)) {
+      const double gv = static_cast<double>(gbar[k]);
+      const double dv = static_cast<double>(xn[k]) - static_cast<double>(xl[k]);
+      acc.gsq += gv * gv;
+      acc.dsq += dv * dv;
+      acc.nf += ((__float_as_uint(xn[k]) & 0x7F800000u) == 0x7F800000u) ? 1u : 0u;
+    }
+  }
+}
+
+// Deterministic block sum: a fixed xor-butterfly inside each wavefront, then the
+// wavefront sums in index order.  Result valid in thread 0.
+template <typename CountT>
+__device__ __forceinline__ AccT<CountT> block_sum(AccT<CountT> v) {
+  __shared__ double s_g[kBlock / 64];
+  __shared__ double s_d[kBlock / 64];
+  __shared__ CountT s_n[kBlock / 64];
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    v.gsq += __shfl_xor(v.gsq, off, 64);
+    v.dsq += __shfl_xor(v.dsq, off, 64);
+    v.nf += __shfl_xor(v.nf, off, 64);
+  }
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    s_g[wave] = v.gsq;
+    s_d[wave] = v.dsq;
+    s_n[wave] = v.nf;
+  }
+  __syncthreads();
+  AccT<CountT> r = {0.0, 0.0, 0};
+  if (threadIdx.x == 0) {
+    for (int w = 0; w < kBlock / 64; ++w) {
+      r.gsq += s_g[w];
+      r.dsq += s_d[w];
+      r.nf += s_n[w];
+    }
+  }
+  __syncthreads();
+  return r;
+}
+
+// ----------------------------------------------------------- one 4-vector
+template <int MODE, int G, int PP, bool FULL, bool STATS>
+__device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned mask, float two_s,
+                                         const Divisor& qg, const Divisor& qm, Acc& acc) {
+  if constexpr (MODE == kModePack) {
+    const f32x4 v = load_f32<FULL, true>(a.src, e0, mask);
+    store_bf16<FULL>(a.wire, e0, mask, pack4(v));
+    return;
+  }
+  const int g = (G > 0) ? G : a.g;
+  const int P = (PP >= 0) ? PP : a.P;
+
+  f32x4 gbar = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (MODE == kModeAvg || MODE == kModeFused) {
+    f32x4 s = load_f32<FULL, true>(a.grads[0], e0, mask);
+#pragma unroll
+    for (int r = 1; r < g; ++r) s = s + load_f32<FULL, true>(a.grads[r], e0, mask);
+    gbar = divide(s, qg);
+    if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
+    if constexpr (MODE == kModeAvg) return;
+  }
+
+  f32x4 x = load_f32<FULL, false>(a.x, e0, mask);
+  f32x4 xl = x;
+  if constexpr (MODE == kModeFused) {
+    const f32x4 m = load_f32<FULL, false>(a.m, e0, mask);
+    f32x4 d = gbar;
+    if (a.wd != 0.0f) d = gbar + (a.wd * x);
+    const f32x4 m_new = (a.mu * m) + d;
+    xl = x - (a.lr * m_new);
+    store_f32<FULL, false>(a.m, e0, mask, m_new);
+  }
+
+  f32x4 xn = xl;
+  if (P > 0) {
+    f32x4 acc4 = two_s * xl;
+#pragma unroll
+    for (int i = 0; i < P; ++i) acc4 = acc4 + widen4(load_bf16<FULL>(a.stale[i], e0, mask));
+    xn = divide(acc4, qm);
+  }
+  store_f32<FULL, false>(a.x, e0, mask, xn);
+  if (a.wire) {
+    const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
+    store_bf16<FULL>(a.wire, e0, mask, pack4(pre ? xl : xn));
+  }
+  if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
+}
+
+// ------------------------------------------------------------------- kernel
+template <int MODE, int G, int PP, bool STATS>
+__global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
+  const int tile = static_cast<int>(blockIdx.x);
+  // bucket owning this tile: the last one whose first tile is <= tile
+  int lo = 0, hi = a.nb - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.b[mid].first_tile <= tile) lo = mid;
+    else hi = mid - 1;
+  }
+  const TileBucket bk = a.b[lo];
+  const int64_t abase = (bk.start & ~int64_t(kVec - 1)) + int64_t(tile - bk.first_tile) * kTile;
+  const int64_t tlo = bk.start > abase ? bk.start : abase;
+  const int64_t thi = bk.end < abase + kTile ? bk.end : abase + kTile;
+
+  const int P = (PP >= 0) ? PP : a.P;
+  const float two_s = static_cast<float>(2 * bk.S);
+  const Divisor qg = make_divisor((G > 0) ? G : a.g);
+  const Divisor qm = make_divisor(2 * bk.S + P);
+
+  Acc acc = {0.0, 0.0, 0u};
+#pragma unroll 2
+  for (int it = 0; it < kIters; ++it) {
+    const int64_t e0 = abase + (int64_t(it) * kBlock + threadIdx.x) * kVec;
+    if (e0 >= tlo && e0 + kVec <= thi) {
+      step_vec<MODE, G, PP, true, STATS>(a, e0, 0xFu, two_s, qg, qm, acc);
+    } else if (e0 + kVec > tlo && e0 < thi) {
+      unsigned mask = 0;
+#pragma unroll
+      for (int k = 0; k < kVec; ++k)
+        if (e0 + k >= tlo && e0 + k < thi) mask |= 1u << k;
+      step_vec<MODE, G, PP, false, STATS>(a, e0, mask, two_s, qg, qm, acc);
+    }
+  }
+
+  if constexpr (STATS && MODE == kModeFused) {
+    // Per-tile partial, then the last workgroup to finish reduces the partials
+    // of each bucket in tile order and clears the counter for the next launch.
+    __shared__ unsigned s_last;
+    const Acc t = block_sum(acc);
+    if (threadIdx.x == 0) {
+      TilePartial* pt = a.partials + tile;
+      __hip_atomic_store(&pt->grad_sq, t.gsq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&pt->delta_sq, t.dsq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&pt->nonfinite, static_cast<uint64_t>(t.nf), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      __threadfence();
+      const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = (prev == static_cast<unsigned>(a.ntiles - 1)) ? 1u : 0u;
+    }
+    __syncthreads();
+    if (s_last) {
+      __threadfence();
+      for (int i = 0; i < a.nb; ++i) {
+        const int t0 = a.b[i].first_tile;
+        const int t1 = (i + 1 < a.nb) ? a.b[i + 1].first_tile : a.ntiles;
+        Acc64 v = {0.0, 0.0, 0};
+        for (int j = t0 + static_cast<int>(threadIdx.x); j < t1; j += kBlock) {
+          const TilePartial* pt = a.partials + j;
+          v.gsq += __hip_atomic_load(&pt->grad_sq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          v.dsq += __hip_atomic_load(&pt->delta_sq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          v.nf += __hip_atomic_load(&pt->nonfinite, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        const Acc64 r = block_sum(v);
+        if (threadIdx.x == 0) {
+          a.stats[i].grad_sq = r.gsq;
+          a.stats[i].delta_sq = r.dsq;
+          a.stats[i].nonfinite = r.nf;
+        }
+      }
+      if (threadIdx.x == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+}
+
+template <int MODE, int G, int PP, bool STATS>
+hipError_t launch(const StepArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS>), dim3(a.ntiles), dim3(kBlock), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <bool STATS>
+hipError_t launch_fused(const StepArgs& a, hipStream_t stream) {
+  // Fully unrolled instances for common (g, P); any other pair takes the
+  // runtime-count instance, which computes the same bits.
+  if (a.g == 4 && a.P == 2) return launch<kModeFused, 4, 2, STATS>(a, stream);
+  if (a.g == 4 && a.P == 4) return launch<kModeFused, 4, 4, STATS>(a, stream);
+  if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS>(a, stream);
+  if (a.g == 4 && a.P == 16) return launch<kModeFused, 4, 16, STATS>(a, stream);
+  if (a.g == 8 && a.P == 32) return launch<kModeFused, 8, 32, STATS>(a, stream);
+  return launch<kModeFused, 0, -1, STATS>(a, stream);
+}
+
+}  // namespace
+
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, hipStream_t stream) {
+  switch (mode) {
+    case kModeAvg:
+      return launch<kModeAvg, 0, -1, false>(a, stream);
+    case kModePack:
+      return launch<kModePack, 0, -1, false>(a, stream);
+    case kModeMerge:
+      return launch<kModeMerge, 0, -1, false>(a, stream);
+    case kModeFused:
+      return with_stats ? launch_fused<true>(a, stream) : launch_fused<false>(a, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace daso

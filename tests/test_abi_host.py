@@ -1,0 +1,165 @@
+"""The C-ABI library without a GPU: it loads, exports every function that
+include/daso.h declares, and rejects bad arguments before anything is launched.
+
+The argument checks run on the host before any HIP call, so they can be fed
+fake (never dereferenced) device addresses.  These tests only ever pass
+arguments that must be rejected; to be certain that nothing is launched on
+real hardware with such addresses, they skip when a GPU is visible."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2104_05588_amd import _lib as L
+from paper_2104_05588_amd import build as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "daso.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        B.build()
+    return L.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(daso_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_fused_sync_step",
+                     "daso_status_string"):
+        assert required in names
+    assert set(names) == set(L.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version(lib):
+    assert lib.daso_abi_version() == 100
+    for code in (L.DASO_OK, L.DASO_EINVAL, L.DASO_EALIGN, L.DASO_EALIAS, L.DASO_EHIP):
+        s = L.status_string(code)
+        assert s.startswith("DASO_")
+    assert "unknown" in L.status_string(-99)
+
+
+def test_struct_layouts_match_header():
+    assert ctypes.sizeof(L.daso_bucket) == 24
+    assert ctypes.sizeof(L.daso_bucket_stats) == 24
+    assert L.daso_sync_args.stats.offset == ctypes.sizeof(L.daso_sync_args) - 8
+
+
+# ------------------------------------------------------------- validation
+def _no_gpu():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("argument-check tests use fake device addresses; run them without a GPU")
+
+
+A = 0x10000000          # fake, 16-byte aligned "device" addresses, never dereferenced
+MB = 1 << 20
+
+
+def ptrs(*xs):
+    arr = (ctypes.c_void_p * max(len(xs), 1))()
+    for i, x in enumerate(xs):
+        arr[i] = x
+    return arr
+
+
+def test_local_avg_rejects(lib):
+    _no_gpu()
+    f, n = lib.daso_local_avg, 1000
+    g4 = ptrs(A, A + MB, A + 2 * MB, A + 3 * MB)
+    assert f(g4, 0, A + 8 * MB, n, None) == L.DASO_EINVAL
+    assert f(g4, 65, A + 8 * MB, n, None) == L.DASO_EINVAL
+    assert f(None, 4, A + 8 * MB, n, None) == L.DASO_EINVAL
+    assert f(g4, 4, None, n, None) == L.DASO_EINVAL
+    assert f(g4, 4, A + 8 * MB, -1, None) == L.DASO_EINVAL
+    assert f(ptrs(A, 0, A + 2 * MB, A + 3 * MB), 4, A + 8 * MB, n, None) == L.DASO_EINVAL
+    assert f(g4, 4, A + 8 * MB + 4, n, None) == L.DASO_EALIGN
+    assert f(ptrs(A, A + MB + 8, A + 2 * MB, A + 3 * MB), 4, A + 8 * MB, n, None) == L.DASO_EALIGN
+    assert f(g4, 4, A + MB + 64, n, None) == L.DASO_EALIAS  # partial overlap with grads[1]
+    assert f(g4, 4, A + 8 * MB, 0, None) == L.DASO_OK       # n == 0: no-op
+
+
+def test_pack_rejects(lib):
+    _no_gpu()
+    f = lib.daso_pack_bf16
+    assert f(A, A + 1008, 1000, None) == L.DASO_EALIAS
+    assert f(A, A + 8 * MB + 2, 1000, None) == L.DASO_EALIGN
+    assert f(None, A + 8 * MB, 1000, None) == L.DASO_EINVAL
+    assert f(A, A + 8 * MB, -5, None) == L.DASO_EINVAL
+    assert f(A, A + 8 * MB, 0, None) == L.DASO_OK
+
+
+def test_global_merge_rejects(lib):
+    _no_gpu()
+    f, n = lib.daso_global_merge, 1000
+    st = ptrs(A + MB, A + 2 * MB)
+    ok_b = L.bucket_table([(0, 600, 1), (600, 400, 2)])
+    assert f(A, st, 2, L.bucket_table([(0, 600, 1), (601, 399, 2)]), 2, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 2, L.bucket_table([(0, 600, 1), (600, 401, 2)]), 2, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 2, L.bucket_table([(0, 600, -1), (600, 400, 2)]), 2, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 2, L.bucket_table([(0, 1000, 1 << 21)]), 1, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 2, ok_b, 0, None, n, None) == L.DASO_EINVAL
+    bad = L.bucket_table([(0, 1000, 1)])
+    bad[0].reserved = 3
+    assert f(A, st, 2, bad, 1, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 65, ok_b, 2, None, n, None) == L.DASO_EINVAL
+    assert f(A, None, 2, ok_b, 2, None, n, None) == L.DASO_EINVAL
+    assert f(A, ptrs(A + 1024, A + 2 * MB), 2, ok_b, 2, None, n, None) == L.DASO_EALIAS
+    assert f(A, st, 2, ok_b, 2, A + 2 * MB + 512, n, None) == L.DASO_EALIAS
+    assert f(A, st, 2, ok_b, 2, A + 3 * MB + 2, n, None) == L.DASO_EALIGN
+    assert f(A + 4, st, 2, ok_b, 2, None, n, None) == L.DASO_EALIGN
+
+
+def _args(n=1000, g=2, P=2):
+    a = L.daso_sync_args()
+    keep = [ptrs(*[A + r * MB for r in range(g)]), ptrs(*[A + (10 + i) * MB for i in range(P)]),
+            L.bucket_table([(0, n, 2)])]
+    a.n, a.g, a.P = n, g, P
+    a.grads, a.stale = keep[0], keep[1]
+    a.params, a.momentum = A + 20 * MB, A + 21 * MB
+    a.wire, a.grad_avg, a.stats = A + 22 * MB, None, None
+    a.buckets, a.nbuckets = keep[2], 1
+    a.lr, a.mu, a.weight_decay, a.flags = 0.1, 0.9, 0.0, 0
+    return a, keep
+
+
+def test_fused_rejects(lib):
+    _no_gpu()
+    f = lib.daso_fused_sync_step
+    assert f(None, None) == L.DASO_EINVAL
+
+    def rc(**kw):
+        a, keep = _args()
+        for k, v in kw.items():
+            setattr(a, k, v)
+        return f(ctypes.byref(a), None)
+
+    assert rc(g=0) == L.DASO_EINVAL
+    assert rc(P=-1) == L.DASO_EINVAL
+    assert rc(flags=4) == L.DASO_EINVAL
+    assert rc(params=None) == L.DASO_EINVAL
+    assert rc(momentum=A + 21 * MB + 4) == L.DASO_EALIGN
+    assert rc(stats=A + 30 * MB + 4) == L.DASO_EALIGN
+    assert rc(momentum=A + 20 * MB + 16) == L.DASO_EALIAS        # params / momentum overlap
+    assert rc(wire=A + 21 * MB + 64) == L.DASO_EALIAS            # wire inside momentum
+    assert rc(wire=A + 10 * MB) == L.DASO_EALIAS                 # wire on a stale copy
+    assert rc(params=A + MB + 32) == L.DASO_EALIAS               # params inside grads[1]
+    assert rc(grad_avg=A + 11 * MB) == L.DASO_EALIAS             # grad_avg on a stale copy
+    assert rc(grad_avg=A + MB + 16) == L.DASO_EALIAS             # partial overlap with grads[1]
+    assert rc(grad_avg=A + 20 * MB) == L.DASO_EALIAS             # grad_avg on params
+    assert rc(stats=A + 22 * MB) == L.DASO_EALIAS                # stats on the wire
+    assert rc(nbuckets=0) == L.DASO_EINVAL
+    assert rc(n=0) == L.DASO_OK

@@ -1,0 +1,415 @@
+"""GPU parity: every C-ABI entry point against the CPU oracle on the same seeded
+inputs.  The bar: bf16 wire and integer outputs bit-exact; fp32 outputs within
+max |err| <= 1e-6 * max(1, |x|), and bit-exact as well, since both sides
+evaluate the same binary32 operations in the same order (NaN payloads aside:
+a NaN must meet a NaN).  Side-output sums are fp64 reductions in different
+orders: relative 1e-10."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2104_05588_amd as daso
+from oracle import daso_oracle as O
+from workloads import recipes as R
+from workloads import generate as Gen
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    daso.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def announce(*what):
+    print("\n[case]", *what, flush=True)
+
+
+# ---------------------------------------------------------------- helpers
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=F32)).to("cuda")
+
+
+def dev_bf16(u16):
+    return torch.from_numpy(np.ascontiguousarray(u16, dtype=np.uint16).view(np.int16)).to("cuda")
+
+
+def host_f32(t):
+    return t.detach().cpu().numpy()
+
+
+def host_u16(t):
+    return t.detach().cpu().numpy().view(np.uint16)
+
+
+def check_f32(got, want, what):
+    got = np.asarray(got, dtype=F32)
+    want = np.asarray(want, dtype=F32)
+    assert got.shape == want.shape, what
+    both_nan = np.isnan(got) & np.isnan(want)
+    fin = np.isfinite(want) & np.isfinite(got)
+    err = np.abs(got[fin].astype(np.float64) - want[fin].astype(np.float64))
+    lim = 1e-6 * np.maximum(1.0, np.abs(want[fin].astype(np.float64)))
+    over = int(np.count_nonzero(err > lim))
+    diff = (got.view(np.uint32) != want.view(np.uint32)) & ~both_nan
+    nd = int(np.count_nonzero(diff))
+    if over or nd:
+        idx = np.nonzero(diff)[0][:6]
+        raise AssertionError(f"{what}: {over} elements beyond 1e-6*max(1,|x|), {nd} of {got.size} "
+                             f"not bit-identical; first at {idx.tolist()}: got {got[idx].tolist()} "
+                             f"want {want[idx].tolist()}")
+
+
+def check_u16(got, want, what):
+    got = np.asarray(got, dtype=np.uint16)
+    want = np.asarray(want, dtype=np.uint16)
+    diff = got != want
+    if diff.any():
+        idx = np.nonzero(diff)[0][:6]
+        raise AssertionError(f"{what}: {int(diff.sum())} of {got.size} differ; first at {idx.tolist()}: "
+                             f"got {[hex(v) for v in got[idx]]} want {[hex(v) for v in want[idx]]}")
+
+
+def check_stats(got, want, what):
+    assert len(got) == len(want), what
+    for b, (g, w) in enumerate(zip(got, want)):
+        for k in (0, 1):
+            if np.isnan(w[k]):
+                assert np.isnan(g[k]), (what, b, k, g, w)
+            elif np.isinf(w[k]):
+                assert g[k] == w[k], (what, b, k, g, w)
+            else:
+                assert abs(g[k] - w[k]) <= 1e-10 * max(abs(w[k]), 1e-300), (what, b, k, g, w)
+        assert g[2] == w[2], (what, b, g, w)
+
+
+def random_buckets(rng, n, nb, S_choices=(0, 1, 2, 3, 4, 8)):
+    """nb buckets with random (mostly unaligned) boundaries tiling [0, n)."""
+    if n == 0:
+        return [(0, 0, 1)]
+    cuts = sorted(set(rng.integers(1, n, size=max(nb - 1, 0)).tolist())) if n > 1 else []
+    edges = [0] + cuts + [n]
+    bks = [(edges[i], edges[i + 1] - edges[i], int(rng.choice(S_choices))) for i in range(len(edges) - 1)]
+    order = rng.permutation(len(bks))  # the ABI takes buckets in any order
+    return [bks[i] for i in order]
+
+
+def random_inputs(rng, n, g, P, specials=False):
+    x = (rng.standard_normal(n) * 0.02).astype(F32)
+    m = (rng.standard_normal(n) * 1e-3).astype(F32)
+    grads = [(rng.standard_normal(n) * 1e-3).astype(F32) for _ in range(g)]
+    stale = [O.bf16_rne(x + (rng.standard_normal(n) * 1e-4).astype(F32)) for _ in range(P)]
+    if specials and n:
+        vals = np.array([np.nan, np.inf, -np.inf, 1e-40, -1e-41, 3.4e38, -3.4e38, -0.0, 0.0,
+                         1.17549435e-38, 2.0 ** -149], dtype=F32)
+        for arr in [x, m] + grads:
+            k = max(1, n // 50)
+            pos = rng.integers(0, n, k)
+            arr[pos] = rng.choice(vals, k)
+        for i in range(P):
+            k = max(1, n // 50)
+            pos = rng.integers(0, n, k)
+            stale[i][pos] = O.bf16_rne(rng.choice(vals, k))
+    return {"params": x, "momentum": m, "grads": grads, "stale": stale}
+
+
+def run_fused(inp, buckets, lr=0.1, mu=0.9, wd=0.0, flags=0, wire=True, gavg="none", stats=True):
+    n = inp["params"].shape[0]
+    grads = [dev_f32(a) for a in inp["grads"]]
+    stale = [dev_bf16(a) for a in inp["stale"]]
+    x = dev_f32(inp["params"])
+    m = dev_f32(inp["momentum"])
+    w = torch.empty(n, dtype=torch.int16, device="cuda") if wire else None
+    ga = grads[0] if gavg == "alias" else (torch.empty(n, dtype=torch.float32, device="cuda")
+                                           if gavg == "new" else None)
+    st = daso.new_stats(len(buckets)) if stats else None
+    daso.fused_sync_step(grads, x, m, stale, buckets, lr, mu, wd, w, ga, st, flags)
+    torch.cuda.synchronize()
+    return {"params": host_f32(x), "momentum": host_f32(m),
+            "wire": host_u16(w) if wire else None,
+            "grad_avg": host_f32(ga) if ga is not None else None,
+            "stats": daso.decode_stats(st) if stats else None}
+
+
+def compare_fused(got, want, what, wire=True, gavg=False, stats=True):
+    check_f32(got["params"], want["params"], what + " params")
+    check_f32(got["momentum"], want["momentum"], what + " momentum")
+    if wire:
+        check_u16(got["wire"], want["wire"], what + " wire")
+    if gavg:
+        check_f32(got["grad_avg"], want["grad_avg"], what + " grad_avg")
+    if stats:
+        check_stats(got["stats"], want["stats"], what + " stats")
+
+
+SIZES = [1, 3, 4, 5, 7, 8, 9, 4095, 4097, 8191, 8192, 8193, 100_003]
+
+
+# ------------------------------------------------------------------ pack
+def test_pack_every_high_half_and_specials():
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF, 0x4000, 0xC000], dtype=np.uint32)
+    u = (hi[:, None] | lows[None, :]).ravel()
+    u = np.concatenate([u, np.random.default_rng(1).integers(0, 1 << 32, 1_000_003, dtype=np.uint64)
+                        .astype(np.uint32)])
+    f = u.view(F32)
+    announce("pack_bf16 n=", f.size)
+    src = dev_f32(f)
+    wire = torch.empty(f.size, dtype=torch.int16, device="cuda")
+    daso.pack_bf16(src, wire)
+    torch.cuda.synchronize()
+    check_u16(host_u16(wire), O.pack_bf16(f), "pack")
+
+
+@pytest.mark.parametrize("n", SIZES)
+def test_pack_sizes(n):
+    announce("pack_bf16 n=", n)
+    f = (np.random.default_rng(n).standard_normal(n) * 3).astype(F32)
+    src = dev_f32(f)
+    wire = torch.full((n + 8,), 0x1234, dtype=torch.int16, device="cuda")
+    daso.pack_bf16(src, wire[:n])
+    torch.cuda.synchronize()
+    h = host_u16(wire)
+    check_u16(h[:n], O.pack_bf16(f), f"pack n={n}")
+    assert np.all(h[n:] == 0x1234), "wrote past the end"
+
+
+# ------------------------------------------------------------ local avg
+@pytest.mark.parametrize("g", [1, 2, 3, 4, 5, 7, 8, 16, 64])
+def test_local_avg(g):
+    rng = np.random.default_rng(100 + g)
+    for n in (1, 7, 8193, 100_003):
+        announce("local_avg g=", g, "n=", n)
+        G = [(rng.standard_normal(n) * 1e-3).astype(F32) for _ in range(g)]
+        gd = [dev_f32(a) for a in G]
+        out = torch.empty(n + 4, dtype=torch.float32, device="cuda").fill_(7.0)
+        daso.local_avg(gd, out[:n])
+        torch.cuda.synchronize()
+        h = host_f32(out)
+        check_f32(h[:n], O.local_avg(G), f"local_avg g={g} n={n}")
+        assert np.all(h[n:] == 7.0)
+        # in place: every replica's gradients become the average (Figure 2)
+        daso.local_avg(gd, gd[0])
+        torch.cuda.synchronize()
+        check_f32(host_f32(gd[0]), O.local_avg(G), f"local_avg in place g={g} n={n}")
+
+
+# ---------------------------------------------------------------- merge
+@pytest.mark.parametrize("P", [0, 1, 2, 3, 8, 17, 32, 64])
+def test_global_merge(P):
+    rng = np.random.default_rng(200 + P)
+    for n in (1, 9, 4097, 300_001):
+        for nb in (1, 5):
+            bks = random_buckets(rng, n, nb)
+            announce("global_merge P=", P, "n=", n, "buckets=", len(bks))
+            x = (rng.standard_normal(n) * 0.02).astype(F32)
+            st = [O.bf16_rne(x + (rng.standard_normal(n) * 1e-4).astype(F32)) for _ in range(P)]
+            want, wire_want = O.global_merge(x, st, bks, pack=True)
+            xd = dev_f32(x)
+            wd = torch.empty(n, dtype=torch.int16, device="cuda")
+            daso.global_merge(xd, [dev_bf16(s) for s in st], bks, wd)
+            torch.cuda.synchronize()
+            check_f32(host_f32(xd), want, f"merge P={P} n={n}")
+            check_u16(host_u16(wd), wire_want, f"merge wire P={P} n={n}")
+            xd2 = dev_f32(x)
+            daso.global_merge(xd2, [dev_bf16(s) for s in st], bks, None)
+            torch.cuda.synchronize()
+            check_f32(host_f32(xd2), want, f"merge no-wire P={P} n={n}")
+
+
+def test_global_merge_many_buckets():
+    """More buckets than one launch carries: the library splits the launches."""
+    rng = np.random.default_rng(300)
+    n, P = 500_000, 6
+    bks = random_buckets(rng, n, 150)
+    announce("global_merge many buckets", len(bks))
+    x = (rng.standard_normal(n) * 0.02).astype(F32)
+    st = [O.bf16_rne(x + (rng.standard_normal(n) * 1e-4).astype(F32)) for _ in range(P)]
+    want, wire_want = O.global_merge(x, st, bks, pack=True)
+    xd = dev_f32(x)
+    wd = torch.empty(n, dtype=torch.int16, device="cuda")
+    daso.global_merge(xd, [dev_bf16(s) for s in st], bks, wd)
+    torch.cuda.synchronize()
+    check_f32(host_f32(xd), want, "merge many")
+    check_u16(host_u16(wd), wire_want, "merge many wire")
+
+
+# ---------------------------------------------------------------- fused
+FUSED_CASES = [
+    # (seed, n, g, P, nbuckets, wd, flags, gavg)
+    (1, 1, 1, 0, 1, 0.0, 0, "none"),
+    (2, 7, 4, 2, 1, 0.0, 0, "new"),
+    (3, 4097, 4, 8, 3, 0.0, 0, "alias"),
+    (4, 8193, 3, 5, 4, 1e-4, 0, "new"),
+    (5, 100_003, 8, 32, 6, 0.0, 0, "none"),
+    (6, 100_003, 2, 0, 2, 1e-4, daso.DASO_PACK_PRE_MERGE, "new"),
+    (7, 65_536, 4, 2, 1, 0.0, daso.DASO_PACK_PRE_MERGE, "none"),
+    (8, 300_007, 5, 17, 9, 1e-4, 0, "alias"),
+    (9, 123_457, 1, 1, 2, 0.0, 0, "none"),
+    (10, 50_001, 64, 64, 3, 0.0, 0, "new"),
+    (11, 77_777, 4, 16, 5, 0.0, 0, "none"),
+    (12, 12_345, 6, 3, 70, 0.0, 0, "none"),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=[f"s{c[0]}_n{c[1]}_g{c[2]}_P{c[3]}" for c in FUSED_CASES])
+def test_fused_random(case):
+    seed, n, g, P, nb, wd, flags, gavg = case
+    rng = np.random.default_rng(seed)
+    bks = random_buckets(rng, n, nb)
+    inp = random_inputs(rng, n, g, P)
+    announce("fused", case, "buckets", len(bks))
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                             0.1, 0.9, wd, flags)
+    got = run_fused(inp, bks, wd=wd, flags=flags, gavg=gavg)
+    compare_fused(got, want, f"fused {case}", gavg=gavg != "none")
+
+
+@pytest.mark.parametrize("seed", [21, 22, 23])
+def test_fused_special_values(seed):
+    """NaN, infinities, subnormals, the largest finite values and signed zeros
+    injected into every input stream."""
+    rng = np.random.default_rng(seed)
+    n, g, P = 20_011, 3, 5
+    bks = random_buckets(rng, n, 4)
+    inp = random_inputs(rng, n, g, P, specials=True)
+    announce("fused specials seed", seed)
+    for wd in (0.0, 1e-4):
+        want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                                 0.1, 0.9, wd)
+        got = run_fused(inp, bks, wd=wd, gavg="new")
+        compare_fused(got, want, f"fused specials seed={seed} wd={wd}", gavg=True)
+        assert sum(s[2] for s in got["stats"]) > 0
+
+
+def test_fused_without_optional_outputs():
+    rng = np.random.default_rng(31)
+    n = 33_333
+    bks = random_buckets(rng, n, 3)
+    inp = random_inputs(rng, n, 4, 4)
+    announce("fused without wire/stats")
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+    got = run_fused(inp, bks, wire=False, stats=False)
+    compare_fused(got, want, "fused bare", wire=False, stats=False)
+
+
+def test_fused_empty_buckets_and_many_launches():
+    rng = np.random.default_rng(32)
+    n = 400_000
+    bks = random_buckets(rng, n, 180) + [(n, 0, 3), (0, 0, 1)]
+    inp = random_inputs(rng, n, 2, 3)
+    announce("fused empty + many buckets", len(bks))
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+    got = run_fused(inp, bks)
+    compare_fused(got, want, "fused many buckets")
+    assert got["stats"][-1] == (0.0, 0.0, 0) and got["stats"][-2] == (0.0, 0.0, 0)
+
+
+def test_fused_is_deterministic_and_stream_ordered():
+    w = R.workload("resnet18")
+    inp = Gen.host_inputs(w)
+    bks = [(b.start, b.numel, b.S) for b in w.buckets]
+    announce("fused determinism resnet18")
+    side = torch.cuda.Stream()
+    outs = []
+    for _ in range(2):
+        grads = [dev_f32(a) for a in inp["grads"]]
+        stale = [dev_bf16(a) for a in inp["stale"]]
+        x, m = dev_f32(inp["params"]), dev_f32(inp["momentum"])
+        wire = torch.empty(w.n, dtype=torch.int16, device="cuda")
+        st = daso.new_stats(len(bks))
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            daso.fused_sync_step(grads, x, m, stale, bks, 0.1, 0.9, 0.0, wire, None, st)
+            res = (x.clone(), wire.clone(), st.clone())
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        outs.append([host_f32(res[0]).view(np.uint32), host_u16(res[1]), host_f32(res[2])])
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------- workloads, full size
+@pytest.mark.parametrize("name", ["tiny", "resnet18", "resnet50", "segnet"])
+def test_fused_workload_full(name):
+    """Element-by-element parity at the full workload size, in the launch
+    configuration the bench times (wire and statistics on)."""
+    w = R.workload(name)
+    announce("fused workload", name, "n=", w.n, "g=", w.g, "P=", w.P)
+    inp = Gen.host_inputs(w)
+    bks = [(b.start, b.numel, b.S) for b in w.buckets]
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                             w.lr, w.mu, w.wd)
+    got = run_fused(inp, bks, lr=w.lr, mu=w.mu, wd=w.wd)
+    del inp
+    compare_fused(got, want, f"workload {name}")
+
+
+def _sample_indices(w, rng, k=1 << 17):
+    idx = set(rng.integers(0, w.n, k).tolist())
+    for b in w.buckets:
+        for d in range(4):
+            idx.update({b.start + d, b.start + b.numel - 1 - d})
+    idx.update({0, w.n - 1})
+    return np.array(sorted(i for i in idx if 0 <= i < w.n), dtype=np.int64)
+
+
+def test_fused_gpt_medium_full_size_sampled():
+    """The 354.8M-parameter, g=8, P=32 workload at full size: inputs made on the
+    device; the oracle recomputes sampled elements (every bucket edge plus
+    random positions) one by one, and the per-bucket statistics are checked
+    against fp64 sums of values recomputed with plain torch operations."""
+    w = R.workload("gpt_medium")
+    announce("fused gpt_medium full size n=", w.n)
+    torch.manual_seed(0)
+    inp = Gen.device_inputs(w)
+    rng = np.random.default_rng(41)
+    idx = _sample_indices(w, rng)
+    it = torch.from_numpy(idx).to("cuda")
+    take = lambda t: t.index_select(0, it).cpu().numpy()  # noqa: E731
+    s_grads = [take(t) for t in inp["grads"]]
+    s_stale = [take(t).view(np.uint16) for t in inp["stale"]]
+    s_x, s_m = take(inp["params"]), take(inp["momentum"])
+    x0 = inp["params"].clone()
+    # per-sample buckets, in sample coordinates
+    order = sorted(w.buckets, key=lambda b: b.start)
+    starts = np.array([b.start for b in order])
+    bid = np.searchsorted(starts, idx, side="right") - 1
+    s_bks, i0 = [], 0
+    for i in range(1, len(idx) + 1):
+        if i == len(idx) or bid[i] != bid[i0]:
+            s_bks.append((i0, i - i0, order[bid[i0]].S))
+            i0 = i
+    bks = [(b.start, b.numel, b.S) for b in w.buckets]
+    wire = torch.empty(w.n, dtype=torch.int16, device="cuda")
+    st = daso.new_stats(len(bks))
+    daso.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                         w.lr, w.mu, w.wd, wire, None, st)
+    torch.cuda.synchronize()
+    want = O.fused_sync_step(s_grads, s_x, s_m, s_stale, s_bks, w.lr, w.mu, w.wd)
+    check_f32(take(inp["params"]), want["params"], "gpt sampled params")
+    check_f32(take(inp["momentum"]), want["momentum"], "gpt sampled momentum")
+    check_u16(take(wire).view(np.uint16), want["wire"], "gpt sampled wire")
+
+    # statistics: fp64 sums of gbar^2 and (x' - xl)^2 per bucket
+    got = daso.decode_stats(st)
+    gsum = inp["grads"][0].clone()
+    for t in inp["grads"][1:]:
+        gsum += t
+    gbar = gsum / float(w.g)
+    del gsum
+    lr_t = torch.tensor(w.lr, dtype=torch.float32, device="cuda")
+    xl = x0 - torch.mul(inp["momentum"], lr_t)
+    for b, bk in enumerate(w.buckets):
+        sl = slice(bk.start, bk.start + bk.numel)
+        gsq = float(torch.sum(gbar[sl].double() ** 2))
+        dsq = float(torch.sum((inp["params"][sl].double() - xl[sl].double()) ** 2))
+        assert abs(got[b][0] - gsq) <= 1e-9 * gsq, (b, got[b], gsq)
+        assert abs(got[b][1] - dsq) <= 1e-9 * dsq, (b, got[b], dsq)
+        assert got[b][2] == 0
