@@ -196,7 +196,7 @@ def main() -> int:
                    "wire": "bf16", "stats": True, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
-                     "kernel": "step_kernel<fused> (one launch per step)",
+                     "kernel": "step_kernel<fused> + stats_kernel tail (one call per step; HIP events bracket both)",
                      "algorithmic_bytes_per_param": bpp, "algorithmic_bytes_per_launch": alg_bytes,
                      "kernel_avg_us": avg_ms * 1e3, "kernel_median_us": med_ms * 1e3,
                      "kernel_cold_median_us": cold[len(cold) // 2] * 1e3,

@@ -52,9 +52,9 @@ int check_buckets(const daso_bucket* b, int32_t nb, int64_t n) {
 }
 
 // ---------------------------------------------------------------- workspace
-// Per (device, stream): a 256-byte counter slot followed by per-tile partials.
-// Allocated on first use and grown when a larger launch needs it; the counter
-// is zeroed once at allocation and the kernel leaves it at zero.
+// Per (device, stream): the per-tile statistics partials of a fused launch.
+// Allocated on first use and grown when a larger launch needs it; every launch
+// writes each partial it later reads, so the contents never need clearing.
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
@@ -81,7 +81,6 @@ int workspace_for(hipStream_t stream, size_t need, void** out) {
       w.ptr = nullptr;
       return DASO_EHIP;
     }
-    if (hipMemsetAsync(w.ptr, 0, bytes, stream) != hipSuccess) return DASO_EHIP;
     w.bytes = bytes;
   }
   *out = w.ptr;
@@ -123,6 +122,30 @@ void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr) {
   a.ntiles = static_cast<int32_t>(std::max<int64_t>(t, 1));
 }
 
+// Compute units of the current device (cached per device).
+int compute_units() {
+  static std::mutex mu;
+  static std::map<int, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(dev);
+  if (it != cache.end()) return it->second;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
+  cache[dev] = n;
+  return n;
+}
+
+// Workgroups for a launch of `ntiles` tiles: one per tile, or a fixed number
+// per compute unit that take the tiles in turn.
+int grid_for(int32_t ntiles) {
+  if (daso::kBlocksPerCU <= 0) return ntiles;
+  const int cus = compute_units();
+  if (cus <= 0) return ntiles;
+  return static_cast<int>(std::min<int64_t>(ntiles, int64_t(cus) * daso::kBlocksPerCU));
+}
+
 int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
                daso_bucket_stats* stats, hipStream_t stream) {
   const std::vector<Group> groups = group_buckets(b, nb);
@@ -132,17 +155,21 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     max_tiles = std::max(max_tiles, gr.ntiles);
   }
   const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
+  int streams = 2;
+  if (mode == daso::kModeAvg) streams = a.g + 1;
+  if (mode == daso::kModeMerge) streams = a.P + 2 + (a.wire ? 1 : 0);
+  if (mode == daso::kModeFused) streams = a.g + a.P + 4 + (a.wire ? 1 : 0) + (a.gavg ? 1 : 0);
+  a.xcd_order = streams >= daso::kXcdOrderMinStreams ? 1 : 0;
   if (with_stats) {
     void* ws = nullptr;
-    const int rc = workspace_for(stream, 256 + static_cast<size_t>(max_tiles) * sizeof(TilePartial), &ws);
+    const int rc = workspace_for(stream, static_cast<size_t>(max_tiles) * sizeof(TilePartial), &ws);
     if (rc != DASO_OK) return rc;
-    a.counter = static_cast<unsigned int*>(ws);
-    a.partials = reinterpret_cast<TilePartial*>(static_cast<char*>(ws) + 256);
+    a.partials = static_cast<TilePartial*>(ws);
   }
   for (const auto& gr : groups) {
     fill_group(a, b, gr);
     a.stats = with_stats ? stats + gr.first : nullptr;
-    if (daso::launch_step(mode, with_stats, a, stream) != hipSuccess) return DASO_EHIP;
+    if (daso::launch_step(mode, with_stats, a, grid_for(a.ntiles), stream) != hipSuccess) return DASO_EHIP;
   }
   return DASO_OK;
 }

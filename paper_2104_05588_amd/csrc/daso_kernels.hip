@@ -238,112 +238,212 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
   if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
 }
 
-// ------------------------------------------------------------------- kernel
-template <int MODE, int G, int PP, bool STATS>
-__global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
-  const int tile = static_cast<int>(blockIdx.x);
-  // bucket owning this tile: the last one whose first tile is <= tile
-  int lo = 0, hi = a.nb - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.b[mid].first_tile <= tile) lo = mid;
-    else hi = mid - 1;
+// ----------------------------------------------- batched fused step (G, P known)
+// All loads of a batch of vectors are issued before the first store, so that a
+// wavefront keeps every stream of several vectors in flight at once (the
+// compiler cannot move later loads above earlier stores by itself: it cannot
+// prove that the streams do not overlap).
+template <int G, int PP>
+struct FusedIn {
+  f32x4 g[G];
+  f32x4 x;
+  f32x4 m;
+  u32x2 s[PP > 0 ? PP : 1];
+};
+
+template <int G, int PP, bool FULL>
+__device__ __forceinline__ void fused_load(const StepArgs& a, int64_t e0, unsigned mask, FusedIn<G, PP>& v) {
+#pragma unroll
+  for (int r = 0; r < G; ++r) v.g[r] = load_f32<FULL, true>(a.grads[r], e0, mask);
+  v.x = load_f32<FULL, kNtParams>(a.x, e0, mask);
+  v.m = load_f32<FULL, kNtParams>(a.m, e0, mask);
+#pragma unroll
+  for (int i = 0; i < PP; ++i) v.s[i] = load_bf16<FULL>(a.stale[i], e0, mask);
+}
+
+template <int G, int PP, bool FULL, bool STATS>
+__device__ __forceinline__ void fused_finish(const StepArgs& a, int64_t e0, unsigned mask, const FusedIn<G, PP>& v,
+                                             float two_s, const Divisor& qg, const Divisor& qm, Acc& acc) {
+  f32x4 s = v.g[0];
+#pragma unroll
+  for (int r = 1; r < G; ++r) s = s + v.g[r];
+  const f32x4 gbar = divide(s, qg);
+  if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
+  f32x4 d = gbar;
+  if (a.wd != 0.0f) d = gbar + (a.wd * v.x);
+  const f32x4 m_new = (a.mu * v.m) + d;
+  const f32x4 xl = v.x - (a.lr * m_new);
+  store_f32<FULL, kNtParams>(a.m, e0, mask, m_new);
+  f32x4 xn = xl;
+  if constexpr (PP > 0) {
+    f32x4 acc4 = two_s * xl;
+#pragma unroll
+    for (int i = 0; i < PP; ++i) acc4 = acc4 + widen4(v.s[i]);
+    xn = divide(acc4, qm);
   }
-  const TileBucket bk = a.b[lo];
-  const int64_t abase = (bk.start & ~int64_t(kVec - 1)) + int64_t(tile - bk.first_tile) * kTile;
-  const int64_t tlo = bk.start > abase ? bk.start : abase;
-  const int64_t thi = bk.end < abase + kTile ? bk.end : abase + kTile;
+  store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
+  if (a.wire) store_bf16<FULL>(a.wire, e0, mask, pack4((a.flags & DASO_PACK_PRE_MERGE) ? xl : xn));
+  if constexpr (STATS) accumulate(acc, gbar, xl, xn, mask);
+}
 
-  const int P = (PP >= 0) ? PP : a.P;
-  const float two_s = static_cast<float>(2 * bk.S);
-  const Divisor qg = make_divisor((G > 0) ? G : a.g);
-  const Divisor qm = make_divisor(2 * bk.S + P);
+// Vectors per batch: as many as DASO_BATCH allows while the batch's input
+// registers stay within about 48 VGPRs per vector.
+template <int G, int PP>
+constexpr int batch_of() {
+  return (4 * G + 8 + 2 * PP) <= 48 ? kBatch : 1;
+}
 
-  Acc acc = {0.0, 0.0, 0u};
-#pragma unroll 2
+// ------------------------------------------------------------------- tiles
+template <int MODE, int G, int PP, bool STATS>
+__device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64_t tlo, int64_t thi, float two_s,
+                                         const Divisor& qg, const Divisor& qm, Acc& acc) {
+  constexpr bool kBatched = (MODE == kModeFused) && G > 0 && PP >= 0;
+  const int64_t t0 = abase + int64_t(threadIdx.x) * kVec;
+  if constexpr (kBatched) {
+    if (tlo == abase && thi == abase + kTile) {
+      constexpr int B = batch_of<G, PP>();
+      static_assert(kIters % B == 0, "batch must divide the iterations");
+      for (int it = 0; it < kIters; it += B) {
+        FusedIn<G, PP> v[B];
+#pragma unroll
+        for (int b = 0; b < B; ++b) fused_load<G, PP, true>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b]);
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+          fused_finish<G, PP, true, STATS>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm, acc);
+      }
+      return;
+    }
+  }
   for (int it = 0; it < kIters; ++it) {
-    const int64_t e0 = abase + (int64_t(it) * kBlock + threadIdx.x) * kVec;
-    if (e0 >= tlo && e0 + kVec <= thi) {
-      step_vec<MODE, G, PP, true, STATS>(a, e0, 0xFu, two_s, qg, qm, acc);
-    } else if (e0 + kVec > tlo && e0 < thi) {
-      unsigned mask = 0;
+    const int64_t e0 = t0 + int64_t(it) * kBlock * kVec;
+    const bool full = e0 >= tlo && e0 + kVec <= thi;
+    unsigned mask = 0xFu;
+    if (!full) {
+      if (e0 + kVec <= tlo || e0 >= thi) continue;
+      mask = 0;
 #pragma unroll
       for (int k = 0; k < kVec; ++k)
         if (e0 + k >= tlo && e0 + k < thi) mask |= 1u << k;
-      step_vec<MODE, G, PP, false, STATS>(a, e0, mask, two_s, qg, qm, acc);
     }
-  }
-
-  if constexpr (STATS && MODE == kModeFused) {
-    // Per-tile partial, then the last workgroup to finish reduces the partials
-    // of each bucket in tile order and clears the counter for the next launch.
-    __shared__ unsigned s_last;
-    const Acc t = block_sum(acc);
-    if (threadIdx.x == 0) {
-      TilePartial* pt = a.partials + tile;
-      __hip_atomic_store(&pt->grad_sq, t.gsq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&pt->delta_sq, t.dsq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&pt->nonfinite, static_cast<uint64_t>(t.nf), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-      __threadfence();
-      const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (prev == static_cast<unsigned>(a.ntiles - 1)) ? 1u : 0u;
-    }
-    __syncthreads();
-    if (s_last) {
-      __threadfence();
-      for (int i = 0; i < a.nb; ++i) {
-        const int t0 = a.b[i].first_tile;
-        const int t1 = (i + 1 < a.nb) ? a.b[i + 1].first_tile : a.ntiles;
-        Acc64 v = {0.0, 0.0, 0};
-        for (int j = t0 + static_cast<int>(threadIdx.x); j < t1; j += kBlock) {
-          const TilePartial* pt = a.partials + j;
-          v.gsq += __hip_atomic_load(&pt->grad_sq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          v.dsq += __hip_atomic_load(&pt->delta_sq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          v.nf += __hip_atomic_load(&pt->nonfinite, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        const Acc64 r = block_sum(v);
-        if (threadIdx.x == 0) {
-          a.stats[i].grad_sq = r.gsq;
-          a.stats[i].delta_sq = r.dsq;
-          a.stats[i].nonfinite = r.nf;
-        }
+    if constexpr (kBatched) {
+      FusedIn<G, PP> v;
+      if (full) {
+        fused_load<G, PP, true>(a, e0, mask, v);
+        fused_finish<G, PP, true, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
+      } else {
+        fused_load<G, PP, false>(a, e0, mask, v);
+        fused_finish<G, PP, false, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
       }
-      if (threadIdx.x == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      if (full) step_vec<MODE, G, PP, true, STATS>(a, e0, mask, two_s, qg, qm, acc);
+      else step_vec<MODE, G, PP, false, STATS>(a, e0, mask, two_s, qg, qm, acc);
     }
   }
 }
 
+// ------------------------------------------------------------------- kernel
+// Workgroups are dispatched to the 8 XCDs of the chip in turn (workgroup w to
+// XCD w % 8).  xcd_ordered renumbers workgroup w so that each XCD walks a
+// contiguous run of the grid: a bijection of [0, grid).
+__device__ __forceinline__ int xcd_ordered(int w, int grid) {
+  const int q = grid >> 3, r = grid & 7, x = w & 7;
+  return x * q + (x < r ? x : r) + (w >> 3);
+}
+
+// Workgroups take tiles w, w + gridDim.x, ...; the grid is either one workgroup
+// per tile or a few workgroups per compute unit.
 template <int MODE, int G, int PP, bool STATS>
-hipError_t launch(const StepArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS>), dim3(a.ntiles), dim3(kBlock), 0, stream, a);
+__global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
+  const int P = (PP >= 0) ? PP : a.P;
+  const Divisor qg = make_divisor((G > 0) ? G : a.g);
+  const int w0 = a.xcd_order ? xcd_ordered(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x))
+                             : static_cast<int>(blockIdx.x);
+  for (int tile = w0; tile < a.ntiles; tile += static_cast<int>(gridDim.x)) {
+    // bucket owning this tile: the last one whose first tile is <= tile
+    int lo = 0, hi = a.nb - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.b[mid].first_tile <= tile) lo = mid;
+      else hi = mid - 1;
+    }
+    const TileBucket bk = a.b[lo];
+    const int64_t abase = (bk.start & ~int64_t(kVec - 1)) + int64_t(tile - bk.first_tile) * kTile;
+    const int64_t tlo = bk.start > abase ? bk.start : abase;
+    const int64_t thi = bk.end < abase + kTile ? bk.end : abase + kTile;
+    const float two_s = static_cast<float>(2 * bk.S);
+    const Divisor qm = make_divisor(2 * bk.S + P);
+
+    Acc acc = {0.0, 0.0, 0u};
+    run_tile<MODE, G, PP, STATS>(a, abase, tlo, thi, two_s, qg, qm, acc);
+    if constexpr (STATS && MODE == kModeFused) {
+      const Acc t = block_sum(acc);
+      if (threadIdx.x == 0) {
+        TilePartial* pt = a.partials + tile;
+        pt->grad_sq = t.gsq;
+        pt->delta_sq = t.dsq;
+        pt->nonfinite = static_cast<uint64_t>(t.nf);
+      }
+    }
+  }
+}
+
+// Statistics of one launch: workgroup i sums the tile partials of bucket i in
+// tile order (a fixed assignment and reduction tree, so the result does not
+// depend on timing).  Runs after step_kernel on the same stream, which makes
+// every partial visible without any fence inside step_kernel.
+__global__ __launch_bounds__(kBlock) void stats_kernel(const StepArgs a) {
+  const int i = static_cast<int>(blockIdx.x);
+  const int t0 = a.b[i].first_tile;
+  const int t1 = (i + 1 < a.nb) ? a.b[i + 1].first_tile : a.ntiles;
+  Acc64 v = {0.0, 0.0, 0};
+#pragma unroll 4
+  for (int j = t0 + static_cast<int>(threadIdx.x); j < t1; j += kBlock) {
+    const TilePartial p = a.partials[j];
+    v.gsq += p.grad_sq;
+    v.dsq += p.delta_sq;
+    v.nf += p.nonfinite;
+  }
+  const Acc64 r = block_sum(v);
+  if (threadIdx.x == 0) {
+    a.stats[i].grad_sq = r.gsq;
+    a.stats[i].delta_sq = r.dsq;
+    a.stats[i].nonfinite = r.nf;
+  }
+}
+
+template <int MODE, int G, int PP, bool STATS>
+hipError_t launch(const StepArgs& a, int grid, hipStream_t stream) {
+  hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS>), dim3(grid), dim3(kBlock), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !STATS) return e;
+  hipLaunchKernelGGL(stats_kernel, dim3(a.nb), dim3(kBlock), 0, stream, a);
   return hipGetLastError();
 }
 
 template <bool STATS>
-hipError_t launch_fused(const StepArgs& a, hipStream_t stream) {
+hipError_t launch_fused(const StepArgs& a, int grid, hipStream_t stream) {
   // Fully unrolled instances for common (g, P); any other pair takes the
   // runtime-count instance, which computes the same bits.
-  if (a.g == 4 && a.P == 2) return launch<kModeFused, 4, 2, STATS>(a, stream);
-  if (a.g == 4 && a.P == 4) return launch<kModeFused, 4, 4, STATS>(a, stream);
-  if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS>(a, stream);
-  if (a.g == 4 && a.P == 16) return launch<kModeFused, 4, 16, STATS>(a, stream);
-  if (a.g == 8 && a.P == 32) return launch<kModeFused, 8, 32, STATS>(a, stream);
-  return launch<kModeFused, 0, -1, STATS>(a, stream);
+  if (a.g == 4 && a.P == 2) return launch<kModeFused, 4, 2, STATS>(a, grid, stream);
+  if (a.g == 4 && a.P == 4) return launch<kModeFused, 4, 4, STATS>(a, grid, stream);
+  if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS>(a, grid, stream);
+  if (a.g == 4 && a.P == 16) return launch<kModeFused, 4, 16, STATS>(a, grid, stream);
+  if (a.g == 8 && a.P == 32) return launch<kModeFused, 8, 32, STATS>(a, grid, stream);
+  return launch<kModeFused, 0, -1, STATS>(a, grid, stream);
 }
 
 }  // namespace
 
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, hipStream_t stream) {
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, int grid, hipStream_t stream) {
   switch (mode) {
     case kModeAvg:
-      return launch<kModeAvg, 0, -1, false>(a, stream);
+      return launch<kModeAvg, 0, -1, false>(a, grid, stream);
     case kModePack:
-      return launch<kModePack, 0, -1, false>(a, stream);
+      return launch<kModePack, 0, -1, false>(a, grid, stream);
     case kModeMerge:
-      return launch<kModeMerge, 0, -1, false>(a, stream);
+      return launch<kModeMerge, 0, -1, false>(a, grid, stream);
     case kModeFused:
-      return with_stats ? launch_fused<true>(a, stream) : launch_fused<false>(a, stream);
+      return with_stats ? launch_fused<true>(a, grid, stream) : launch_fused<false>(a, grid, stream);
   }
   return hipErrorInvalidValue;
 }

@@ -12,12 +12,34 @@ namespace daso {
 // Work decomposition.  A launch covers up to kLaunchBuckets buckets.  Each bucket
 // [start, end) is cut into tiles of kTile elements aligned to kVec-element
 // vectors (the first tile of a bucket starts at the bucket start rounded down to
-// a vector boundary and is clipped to the bucket); one 256-thread workgroup
-// processes one tile, kIters vectors of kVec elements per thread.
-constexpr int kBlock = 256;
+// a vector boundary and is clipped to the bucket); a 256-thread workgroup
+// processes a tile as kIters vectors of kVec elements per thread.
+// Tuning parameters (compile-time; the defaults are the measured best on MI355X).
+#ifndef DASO_TILE_ITERS
+#define DASO_TILE_ITERS 2
+#endif
+#ifndef DASO_BATCH
+#define DASO_BATCH 2
+#endif
+#ifndef DASO_BLOCKS_PER_CU
+#define DASO_BLOCKS_PER_CU 0
+#endif
+#ifndef DASO_NT_PARAMS
+#define DASO_NT_PARAMS 1
+#endif
+#ifndef DASO_BLOCK
+#define DASO_BLOCK 256
+#endif
+constexpr int kBlock = DASO_BLOCK;
 constexpr int kVec = 4;
-constexpr int kIters = 8;
-constexpr int64_t kTile = int64_t(kBlock) * kVec * kIters;  // 8192 elements
+constexpr int kIters = DASO_TILE_ITERS;
+constexpr int kBatch = DASO_BATCH;           // vectors whose loads are issued together
+constexpr int kBlocksPerCU = DASO_BLOCKS_PER_CU;  // 0: one workgroup per tile
+constexpr bool kNtParams = DASO_NT_PARAMS != 0;   // non-temporal access to params/momentum
+// Streams (inputs + outputs) from which each XCD is given a contiguous run of
+// tiles; measured: a gain with 42 streams, a loss with 17 and 25.
+constexpr int kXcdOrderMinStreams = 32;
+constexpr int64_t kTile = int64_t(kBlock) * kVec * kIters;
 constexpr int kLaunchBuckets = 64;
 
 enum Mode : int { kModeAvg = 0, kModePack = 1, kModeMerge = 2, kModeFused = 3 };
@@ -29,7 +51,7 @@ struct TileBucket {
   int32_t S;           // staleness of Eq. (1)
 };
 
-// Per-tile side-output partial, reduced per bucket by the last workgroup.
+// Per-tile side-output partial, reduced per bucket by stats_kernel.
 struct TilePartial {
   double grad_sq;
   double delta_sq;
@@ -47,7 +69,6 @@ struct StepArgs {
   float* gavg;           // local average output or nullptr
   TilePartial* partials; // per-tile partials (stats only)
   daso_bucket_stats* stats;  // per-bucket outputs (stats only), already offset to this launch
-  unsigned int* counter; // finished-workgroup counter (stats only), zero between launches
   int32_t g;
   int32_t P;
   float lr;
@@ -56,6 +77,7 @@ struct StepArgs {
   uint32_t flags;
   int32_t nb;            // buckets in this launch
   int32_t ntiles;        // tiles in this launch
+  int32_t xcd_order;     // nonzero: renumber workgroups XCD-contiguously
   TileBucket b[kLaunchBuckets];
 };
 
@@ -66,7 +88,8 @@ inline int64_t tiles_of(int64_t start, int64_t end) {
   return (end - a + kTile - 1) / kTile;
 }
 
-// Enqueue one launch of `mode` over the buckets in `args` (grid = args.ntiles).
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, hipStream_t stream);
+// Enqueue one launch of `mode` over the buckets in `args` with `grid`
+// workgroups (1 <= grid <= args.ntiles), which take the tiles in turn.
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, int grid, hipStream_t stream);
 
 }  // namespace daso
