@@ -172,6 +172,32 @@ def main() -> int:
     copy_gbps = 10 * 2 * cp_src.numel() * 4 / (cs.elapsed_time(ce) * 1e-3) / 1e9
     del cp_src, cp_dst
 
+    # the three separate entry points on the same workload, for context
+    def time_call(fn, reps=20):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        ts.sort()
+        return ts[len(ts) // 2] * 1e-3
+
+    gavg = torch.empty(n, dtype=torch.float32, device="cuda")
+    t_avg = time_call(lambda: daso.local_avg(inp["grads"], gavg))
+    t_pack = time_call(lambda: daso.pack_bf16(inp["params"], wire))
+    t_merge = time_call(lambda: daso.global_merge(inp["params"], inp["stale"], bks, wire))
+    del gavg
+    entry_points = {
+        "daso_local_avg": {"us": t_avg * 1e6, "GBps": n * (4 * w.g + 4) / t_avg / 1e9},
+        "daso_pack_bf16": {"us": t_pack * 1e6, "GBps": n * 6 / t_pack / 1e9},
+        "daso_global_merge+wire": {"us": t_merge * 1e6, "GBps": n * (10 + 2 * w.P) / t_merge / 1e9},
+    }
+
     bpp = R.algorithmic_bytes_per_param(w.g, w.P)
     alg_bytes = n * bpp
     achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
@@ -202,6 +228,7 @@ def main() -> int:
                      "kernel_cold_median_us": cold[len(cold) // 2] * 1e3,
                      "cold_frac": alg_bytes / (cold[len(cold) // 2] * 1e-3) / 1e9 / PEAK_HBM_GBPS,
                      "device_copy_GBps": copy_gbps},
+        "entry_points": entry_points,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

@@ -238,78 +238,111 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
   if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
 }
 
-// ----------------------------------------------- batched fused step (G, P known)
+// ------------------------------------- batched vectors (stream counts known)
 // All loads of a batch of vectors are issued before the first store, so that a
 // wavefront keeps every stream of several vectors in flight at once (the
 // compiler cannot move later loads above earlier stores by itself: it cannot
 // prove that the streams do not overlap).
-template <int G, int PP>
-struct FusedIn {
-  f32x4 g[G];
-  f32x4 x;
-  f32x4 m;
-  u32x2 s[PP > 0 ? PP : 1];
+template <int MODE, int G, int PP>
+struct VecIn {
+  static constexpr int kG = (MODE == kModeAvg || MODE == kModeFused) ? G : 0;
+  static constexpr int kP = (MODE == kModeMerge || MODE == kModeFused) ? PP : 0;
+  f32x4 g[kG > 0 ? kG : 1];
+  f32x4 x;  // params (merge, fused) or the source (pack)
+  f32x4 m;  // momentum (fused)
+  u32x2 s[kP > 0 ? kP : 1];
 };
 
-template <int G, int PP, bool FULL>
-__device__ __forceinline__ void fused_load(const StepArgs& a, int64_t e0, unsigned mask, FusedIn<G, PP>& v) {
+template <int MODE, int G, int PP, bool FULL>
+__device__ __forceinline__ void load_in(const StepArgs& a, int64_t e0, unsigned mask, VecIn<MODE, G, PP>& v) {
+  using V = VecIn<MODE, G, PP>;
 #pragma unroll
-  for (int r = 0; r < G; ++r) v.g[r] = load_f32<FULL, true>(a.grads[r], e0, mask);
-  v.x = load_f32<FULL, kNtParams>(a.x, e0, mask);
-  v.m = load_f32<FULL, kNtParams>(a.m, e0, mask);
+  for (int r = 0; r < V::kG; ++r) v.g[r] = load_f32<FULL, true>(a.grads[r], e0, mask);
+  if constexpr (MODE == kModePack) v.x = load_f32<FULL, true>(a.src, e0, mask);
+  if constexpr (MODE == kModeMerge || MODE == kModeFused) v.x = load_f32<FULL, kNtParams>(a.x, e0, mask);
+  if constexpr (MODE == kModeFused) v.m = load_f32<FULL, kNtParams>(a.m, e0, mask);
 #pragma unroll
-  for (int i = 0; i < PP; ++i) v.s[i] = load_bf16<FULL>(a.stale[i], e0, mask);
+  for (int i = 0; i < V::kP; ++i) v.s[i] = load_bf16<FULL>(a.stale[i], e0, mask);
 }
 
-template <int G, int PP, bool FULL, bool STATS>
-__device__ __forceinline__ void fused_finish(const StepArgs& a, int64_t e0, unsigned mask, const FusedIn<G, PP>& v,
-                                             float two_s, const Divisor& qg, const Divisor& qm, Acc& acc) {
-  f32x4 s = v.g[0];
+template <int MODE, int G, int PP, bool FULL, bool STATS>
+__device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned mask, const VecIn<MODE, G, PP>& v,
+                                       float two_s, const Divisor& qg, const Divisor& qm, Acc& acc) {
+  using V = VecIn<MODE, G, PP>;
+  if constexpr (MODE == kModePack) {
+    store_bf16<FULL>(a.wire, e0, mask, pack4(v.x));
+    return;
+  }
+  f32x4 gbar = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (V::kG > 0) {
+    f32x4 s = v.g[0];
 #pragma unroll
-  for (int r = 1; r < G; ++r) s = s + v.g[r];
-  const f32x4 gbar = divide(s, qg);
-  if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
-  f32x4 d = gbar;
-  if (a.wd != 0.0f) d = gbar + (a.wd * v.x);
-  const f32x4 m_new = (a.mu * v.m) + d;
-  const f32x4 xl = v.x - (a.lr * m_new);
-  store_f32<FULL, kNtParams>(a.m, e0, mask, m_new);
+    for (int r = 1; r < V::kG; ++r) s = s + v.g[r];
+    gbar = divide(s, qg);
+    if constexpr (MODE == kModeAvg) {
+      store_f32<FULL, true>(a.gavg, e0, mask, gbar);
+      return;
+    }
+    if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
+  }
+  f32x4 xl = v.x;
+  if constexpr (MODE == kModeFused) {
+    f32x4 d = gbar;
+    if (a.wd != 0.0f) d = gbar + (a.wd * v.x);
+    const f32x4 m_new = (a.mu * v.m) + d;
+    xl = v.x - (a.lr * m_new);
+    store_f32<FULL, kNtParams>(a.m, e0, mask, m_new);
+  }
   f32x4 xn = xl;
-  if constexpr (PP > 0) {
+  if constexpr (V::kP > 0) {
     f32x4 acc4 = two_s * xl;
 #pragma unroll
-    for (int i = 0; i < PP; ++i) acc4 = acc4 + widen4(v.s[i]);
+    for (int i = 0; i < V::kP; ++i) acc4 = acc4 + widen4(v.s[i]);
     xn = divide(acc4, qm);
   }
   store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
-  if (a.wire) store_bf16<FULL>(a.wire, e0, mask, pack4((a.flags & DASO_PACK_PRE_MERGE) ? xl : xn));
-  if constexpr (STATS) accumulate(acc, gbar, xl, xn, mask);
+  if (a.wire) {
+    const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
+    store_bf16<FULL>(a.wire, e0, mask, pack4(pre ? xl : xn));
+  }
+  if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
+}
+
+// Whether an instance has compile-time stream counts (and so the batched path).
+template <int MODE, int G, int PP>
+constexpr bool batched() {
+  if constexpr (MODE == kModePack) return true;
+  if constexpr (MODE == kModeAvg) return G > 0;
+  if constexpr (MODE == kModeMerge) return PP >= 0;
+  return G > 0 && PP >= 0;
 }
 
 // Vectors per batch: as many as DASO_BATCH allows while the batch's input
 // registers stay within about 48 VGPRs per vector.
-template <int G, int PP>
+template <int MODE, int G, int PP>
 constexpr int batch_of() {
-  return (4 * G + 8 + 2 * PP) <= 48 ? kBatch : 1;
+  using V = VecIn<MODE, G, PP>;
+  constexpr int regs = 4 * V::kG + 2 * V::kP + ((MODE == kModeFused) ? 8 : 4);
+  return regs <= 48 ? kBatch : 1;
 }
 
 // ------------------------------------------------------------------- tiles
 template <int MODE, int G, int PP, bool STATS>
 __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64_t tlo, int64_t thi, float two_s,
                                          const Divisor& qg, const Divisor& qm, Acc& acc) {
-  constexpr bool kBatched = (MODE == kModeFused) && G > 0 && PP >= 0;
+  constexpr bool kBatched = batched<MODE, G, PP>();
   const int64_t t0 = abase + int64_t(threadIdx.x) * kVec;
   if constexpr (kBatched) {
     if (tlo == abase && thi == abase + kTile) {
-      constexpr int B = batch_of<G, PP>();
+      constexpr int B = batch_of<MODE, G, PP>();
       static_assert(kIters % B == 0, "batch must divide the iterations");
       for (int it = 0; it < kIters; it += B) {
-        FusedIn<G, PP> v[B];
+        VecIn<MODE, G, PP> v[B];
 #pragma unroll
-        for (int b = 0; b < B; ++b) fused_load<G, PP, true>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b]);
+        for (int b = 0; b < B; ++b) load_in<MODE, G, PP, true>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b]);
 #pragma unroll
         for (int b = 0; b < B; ++b)
-          fused_finish<G, PP, true, STATS>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm, acc);
+          finish<MODE, G, PP, true, STATS>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm, acc);
       }
       return;
     }
@@ -326,13 +359,13 @@ __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64
         if (e0 + k >= tlo && e0 + k < thi) mask |= 1u << k;
     }
     if constexpr (kBatched) {
-      FusedIn<G, PP> v;
+      VecIn<MODE, G, PP> v;
       if (full) {
-        fused_load<G, PP, true>(a, e0, mask, v);
-        fused_finish<G, PP, true, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
+        load_in<MODE, G, PP, true>(a, e0, mask, v);
+        finish<MODE, G, PP, true, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
       } else {
-        fused_load<G, PP, false>(a, e0, mask, v);
-        fused_finish<G, PP, false, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
+        load_in<MODE, G, PP, false>(a, e0, mask, v);
+        finish<MODE, G, PP, false, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
       }
     } else {
       if (full) step_vec<MODE, G, PP, true, STATS>(a, e0, mask, two_s, qg, qm, acc);
@@ -437,11 +470,25 @@ hipError_t launch_fused(const StepArgs& a, int grid, hipStream_t stream) {
 hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, int grid, hipStream_t stream) {
   switch (mode) {
     case kModeAvg:
-      return launch<kModeAvg, 0, -1, false>(a, grid, stream);
+      switch (a.g) {
+        case 1: return launch<kModeAvg, 1, -1, false>(a, grid, stream);
+        case 2: return launch<kModeAvg, 2, -1, false>(a, grid, stream);
+        case 4: return launch<kModeAvg, 4, -1, false>(a, grid, stream);
+        case 8: return launch<kModeAvg, 8, -1, false>(a, grid, stream);
+        default: return launch<kModeAvg, 0, -1, false>(a, grid, stream);
+      }
     case kModePack:
       return launch<kModePack, 0, -1, false>(a, grid, stream);
     case kModeMerge:
-      return launch<kModeMerge, 0, -1, false>(a, grid, stream);
+      switch (a.P) {
+        case 0: return launch<kModeMerge, 0, 0, false>(a, grid, stream);
+        case 2: return launch<kModeMerge, 0, 2, false>(a, grid, stream);
+        case 4: return launch<kModeMerge, 0, 4, false>(a, grid, stream);
+        case 8: return launch<kModeMerge, 0, 8, false>(a, grid, stream);
+        case 16: return launch<kModeMerge, 0, 16, false>(a, grid, stream);
+        case 32: return launch<kModeMerge, 0, 32, false>(a, grid, stream);
+        default: return launch<kModeMerge, 0, -1, false>(a, grid, stream);
+      }
     case kModeFused:
       return with_stats ? launch_fused<true>(a, grid, stream) : launch_fused<false>(a, grid, stream);
   }

@@ -201,7 +201,7 @@ def test_local_avg(g):
 
 
 # ---------------------------------------------------------------- merge
-@pytest.mark.parametrize("P", [0, 1, 2, 3, 8, 17, 32, 64])
+@pytest.mark.parametrize("P", [0, 1, 2, 3, 4, 8, 16, 17, 32, 64])
 def test_global_merge(P):
     rng = np.random.default_rng(200 + P)
     for n in (1, 9, 4097, 300_001):
