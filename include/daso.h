@@ -41,7 +41,8 @@
  *    only; the caller may free or reuse them as soon as the call returns.
  *  - Work is enqueued on `stream` (0 = the null stream) and runs asynchronously;
  *    no call synchronises the device or the stream.
- *  - n == 0 is a valid no-op.
+ *  - n == 0 is a valid no-op: after the checks that do not involve n, the call
+ *    returns DASO_OK and touches no buffer (statistics included).
  *  - On any error nothing is launched and a negative status is returned; the
  *    buffers are untouched.  daso_status_string names the status.
  *  - Calls may be made from several host threads.  Fused steps with statistics
@@ -72,6 +73,9 @@ extern "C" {
 
 /* flags of daso_sync_args */
 #define DASO_PACK_PRE_MERGE 1u /* pack xl (after the optimizer step, before Eq. (1)) instead of x' */
+#define DASO_EXCHANGE_F32 2u   /* fp32 exchange: copies arrive in stale_f32 and the wire is
+                                  wire_f32, both binary32 (no cast; the non-blocking case of
+                                  Section 3); stale and wire must then be NULL */
 
 /* A bucket: elements [start, start + numel) merged with staleness S (S >= 0).
  * S is the number of batches the exchanged copies are late (Eq. (1)); S = 0
@@ -113,8 +117,12 @@ typedef struct daso_sync_args {
   float lr;                        /* learning rate */
   float mu;                        /* momentum factor */
   float weight_decay;              /* coupled L2 term; 0 skips it */
-  uint32_t flags;                  /* DASO_PACK_PRE_MERGE or 0 */
+  uint32_t flags;                  /* DASO_PACK_PRE_MERGE | DASO_EXCHANGE_F32, or 0 */
   daso_bucket_stats* stats;        /* device array of nbuckets entries written, or NULL */
+  const float* const* stale_f32;   /* with DASO_EXCHANGE_F32: host array of P device pointers,
+                                      each n fp32; otherwise NULL */
+  float* wire_f32;                 /* with DASO_EXCHANGE_F32: n fp32 written with x' (or xl), or
+                                      NULL; otherwise NULL */
 } daso_sync_args;
 
 /* Local synchronisation (Section 3, Figure 2): out[j] = (sum_r grads[r][j]) / g,
@@ -138,6 +146,13 @@ int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P,
                       const daso_bucket* buckets, int32_t nbuckets, uint16_t* wire,
                       int64_t n, hipStream_t stream);
 
+/* Eq. (1) for the fp32 exchange (Section 3: in the non-blocking case the
+ * parameters travel uncast): as daso_global_merge, with P fp32 copies, and wire
+ * (NULL, or n fp32) receiving the merged parameters. */
+int daso_global_merge_f32(float* params, const float* const* stale, int32_t P,
+                          const daso_bucket* buckets, int32_t nbuckets, float* wire,
+                          int64_t n, hipStream_t stream);
+
 /* One DASO synchronisation step for one GPU's parameters, in a single pass over
  * memory: local gradient average, SGD-momentum step, Eq. (1) merge per bucket,
  * bf16 pack and (optionally) the per-bucket statistics.  Aliasing rules: params
@@ -145,6 +160,19 @@ int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P,
  * buffer; wire, stats and grad_avg (apart from the allowed grads alias) must not
  * overlap anything else; inputs may overlap each other. */
 int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
+
+/* Bucket plan for a flat parameter buffer (host only, no device work).  The
+ * tensors of a model lie end to end in forward order with element counts
+ * numels[0..ntensors).  Buckets are filled walking the tensors from the last to
+ * the first, as gradients become ready in backpropagation, and a bucket closes
+ * as soon as it holds at least cap_elems elements; what is left forms the last
+ * bucket (tensor fusion / bucketing, Sections 2 and 4).  Bucket b of that walk
+ * gets S = S_cycle[b % n_cycle].  Writes min(count, out_cap) buckets to out (out
+ * may be NULL when out_cap == 0) and returns the bucket count, or DASO_EINVAL
+ * for a negative element count, cap_elems < 1, n_cycle < 1, a negative S or a
+ * null array that is needed.  Buckets never split a tensor. */
+int32_t daso_plan_buckets(const int64_t* numels, int32_t ntensors, int64_t cap_elems,
+                          const int32_t* S_cycle, int32_t n_cycle, daso_bucket* out, int32_t out_cap);
 
 /* Static, NUL-terminated description of a status code. */
 const char* daso_status_string(int status);

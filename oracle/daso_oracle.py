@@ -30,6 +30,10 @@ order so that a GPU implementation can reproduce the same bits:
      16-bit type while the send buffer is packed and cast back on receipt;
      Section 4: DASO uses bfloat16): wire = bf16_rne(x').
 
+The fp32 exchange (Section 3: in the non-blocking case casting does not pay,
+since it delays the start of the communication) keeps the same arithmetic with
+binary32 copies: widen() is the identity and the wire is x' itself.
+
 Readings taken where the paper is silent (each also listed in the design
 notes of the repository): the local state entering Eq. (1) is the state after
 this batch's optimizer step; S is per bucket; the momentum buffer is neither
@@ -104,9 +108,21 @@ def sgd_momentum(x: np.ndarray, m: np.ndarray, gbar: np.ndarray,
     return xl, m_new
 
 
+def _received(st: np.ndarray) -> np.ndarray:
+    """An exchanged state as binary32: bf16 patterns (uint16) are widened
+    exactly, binary32 copies (fp32 exchange) are taken as they are."""
+    st = np.asarray(st)
+    if st.dtype == np.float32:
+        return st
+    if st.dtype != np.uint16:
+        raise TypeError("exchanged states are uint16 bf16 patterns or float32")
+    return bf16_widen(st)
+
+
 def merge_eq1(xl: np.ndarray, stale: Sequence[np.ndarray], S: int) -> np.ndarray:
     """Eq. (1): staleness-weighted average of the local state xl with the P
-    exchanged states (bf16 bit patterns), local weight 2S, each copy weight 1."""
+    exchanged states (bf16 bit patterns or fp32), local weight 2S, each copy
+    weight 1."""
     if S < 0:
         raise ValueError("S must be >= 0")
     P = len(stale)
@@ -115,7 +131,7 @@ def merge_eq1(xl: np.ndarray, stale: Sequence[np.ndarray], S: int) -> np.ndarray
         return xl.copy()
     a = F32(2 * S) * xl
     for st in stale:
-        a = a + bf16_widen(st)
+        a = a + _received(st)
     return a / F32(2 * S + P)
 
 
@@ -139,30 +155,51 @@ def pack_bf16(x: np.ndarray) -> np.ndarray:
     return bf16_rne(x)
 
 
+def _pack(x: np.ndarray, exchange: str) -> np.ndarray:
+    if exchange == "bf16":
+        return bf16_rne(x)
+    if exchange == "f32":
+        return np.array(x, dtype=np.float32, copy=True)
+    raise ValueError("exchange is 'bf16' or 'f32'")
+
+
 def global_merge(params: np.ndarray, stale: Sequence[np.ndarray],
                  buckets: Sequence[Tuple[int, int, int]],
-                 pack: bool = False) -> Tuple[np.ndarray, Optional[np.ndarray]]:
+                 pack: bool = False, exchange: str = "bf16") -> Tuple[np.ndarray, Optional[np.ndarray]]:
     """Eq. (1) applied bucket by bucket with each bucket's own S; optionally
-    packs the merged parameters.  Returns (x', wire or None)."""
+    packs the merged parameters in the exchange type.  Returns (x', wire or None)."""
     x = np.asarray(params, dtype=np.float32)
     n = x.shape[0]
     _check_buckets(n, buckets)
+    _check_exchange(stale, exchange)
     out = np.empty(n, np.float32)
     for (s, k, S) in buckets:
         sl = slice(int(s), int(s) + int(k))
         out[sl] = merge_eq1(x[sl], [st[sl] for st in stale], int(S))
-    return out, (bf16_rne(out) if pack else None)
+    return out, (_pack(out, exchange) if pack else None)
+
+
+def _check_exchange(stale: Sequence[np.ndarray], exchange: str) -> None:
+    want = {"bf16": np.uint16, "f32": np.float32}.get(exchange)
+    if want is None:
+        raise ValueError("exchange is 'bf16' or 'f32'")
+    for st in stale:
+        if np.asarray(st).dtype != want:
+            raise TypeError(f"{exchange} exchange takes {np.dtype(want).name} copies")
 
 
 def fused_sync_step(grads: Sequence[np.ndarray], params: np.ndarray, momentum: np.ndarray,
                     stale: Sequence[np.ndarray], buckets: Sequence[Tuple[int, int, int]],
-                    lr: float, mu: float, wd: float = 0.0, flags: int = 0) -> Dict[str, object]:
+                    lr: float, mu: float, wd: float = 0.0, flags: int = 0,
+                    exchange: str = "bf16") -> Dict[str, object]:
     """One DASO synchronisation step for one GPU's parameters: local gradient
-    average, SGD-momentum step, Eq. (1) merge per bucket, bf16 pack, and the
-    per-bucket side outputs.  Inputs are not modified."""
+    average, SGD-momentum step, Eq. (1) merge per bucket, pack for the exchange
+    (bf16, or fp32 for the non-blocking path), and the per-bucket side outputs.
+    Inputs are not modified."""
     x = np.asarray(params, dtype=np.float32)
     n = x.shape[0]
     _check_buckets(n, buckets)
+    _check_exchange(stale, exchange)
     gbar = local_avg(grads)
     xl, m_new = sgd_momentum(x, momentum, gbar, lr, mu, wd)
     x_new = np.empty(n, np.float32)
@@ -171,7 +208,7 @@ def fused_sync_step(grads: Sequence[np.ndarray], params: np.ndarray, momentum: n
         sl = slice(int(s), int(s) + int(k))
         x_new[sl] = merge_eq1(xl[sl], [st[sl] for st in stale], int(S))
         stats.append(bucket_stats(gbar[sl], xl[sl], x_new[sl]))
-    wire = bf16_rne(xl if (flags & PACK_PRE_MERGE) else x_new)
+    wire = _pack(xl if (flags & PACK_PRE_MERGE) else x_new, exchange)
     return {"params": x_new, "momentum": m_new, "wire": wire, "grad_avg": gbar,
             "x_local": xl, "stats": stats}
 

@@ -4,5 +4,5 @@ The computation lives in libdaso.so (hand-written HIP kernels behind the C ABI
 of include/daso.h); this package holds the build script and a ctypes binding
 that only marshals arguments."""
 from ._lib import (local_avg, pack_bf16, global_merge, fused_sync_step, FusedStep,  # noqa: F401
-                   new_stats, decode_stats, bucket_table, load, status_string, DasoError,
+                   new_stats, decode_stats, bucket_table, plan_buckets, load, status_string, DasoError,
                    DASO_PACK_PRE_MERGE, LIB_PATH, EXPORTED)

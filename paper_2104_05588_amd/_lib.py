@@ -24,9 +24,11 @@ DASO_EHIP = -4
 DASO_MAX_G = 64
 DASO_MAX_P = 64
 DASO_PACK_PRE_MERGE = 1
+DASO_EXCHANGE_F32 = 2
 
-EXPORTED = ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_fused_sync_step",
-            "daso_status_string", "daso_abi_version")
+EXPORTED = ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
+            "daso_fused_sync_step", "daso_plan_buckets", "daso_status_string", "daso_abi_version")
+BUCKET_CAP_ELEMS = 25 * 1024 * 1024 // 4  # 25 MiB of fp32
 
 
 class daso_bucket(ctypes.Structure):
@@ -48,6 +50,7 @@ class daso_sync_args(ctypes.Structure):
         ("buckets", ctypes.POINTER(daso_bucket)), ("nbuckets", ctypes.c_int32),
         ("lr", ctypes.c_float), ("mu", ctypes.c_float), ("weight_decay", ctypes.c_float),
         ("flags", ctypes.c_uint32), ("stats", ctypes.c_void_p),
+        ("stale_f32", ctypes.POINTER(ctypes.c_void_p)), ("wire_f32", ctypes.c_void_p),
     ]
 
 
@@ -75,12 +78,16 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.daso_pack_bf16.argtypes = [vp, vp, i64, vp]
     lib.daso_global_merge.argtypes = [vp, ctypes.POINTER(vp), i32, ctypes.POINTER(daso_bucket), i32,
                                       vp, i64, vp]
+    lib.daso_global_merge_f32.argtypes = lib.daso_global_merge.argtypes
     lib.daso_fused_sync_step.argtypes = [ctypes.POINTER(daso_sync_args), vp]
+    lib.daso_plan_buckets.argtypes = [ctypes.POINTER(i64), i32, i64, ctypes.POINTER(i32), i32,
+                                      ctypes.POINTER(daso_bucket), i32]
+    lib.daso_plan_buckets.restype = i32
     lib.daso_status_string.argtypes = [ctypes.c_int]
     lib.daso_status_string.restype = ctypes.c_char_p
     lib.daso_abi_version.argtypes = []
-    for name in ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_fused_sync_step",
-                 "daso_abi_version"):
+    for name in ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
+                 "daso_fused_sync_step", "daso_abi_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -126,6 +133,21 @@ def bucket_table(buckets: Sequence[Tuple[int, int, int]]):
     return arr
 
 
+def plan_buckets(numels: Sequence[int], cap: int = BUCKET_CAP_ELEMS,
+                 S_cycle: Sequence[int] = (1,)) -> List[Tuple[int, int, int]]:
+    """Bucket plan of a flat buffer of tensors (see daso_plan_buckets):
+    (start, numel, S) per bucket, in walk order (last tensor first)."""
+    lib = load()
+    nt = len(numels)
+    arr = (ctypes.c_int64 * max(nt, 1))(*[int(k) for k in numels])
+    cyc = (ctypes.c_int32 * max(len(S_cycle), 1))(*[int(S) for S in S_cycle])
+    count = lib.daso_plan_buckets(arr, nt, int(cap), cyc, len(S_cycle), None, 0)
+    _check(min(count, 0), "daso_plan_buckets")
+    out = (daso_bucket * max(count, 1))()
+    lib.daso_plan_buckets(arr, nt, int(cap), cyc, len(S_cycle), out, count)
+    return [(out[i].start, out[i].numel, out[i].S) for i in range(count)]
+
+
 def _check(rc: int, what: str) -> None:
     if rc != DASO_OK:
         raise DasoError(rc, what)
@@ -149,16 +171,25 @@ def pack_bf16(src: torch.Tensor, wire: torch.Tensor, stream=None) -> torch.Tenso
     return wire
 
 
+def _is_f32_exchange(stale: Sequence[torch.Tensor], wire: Optional[torch.Tensor]) -> bool:
+    """fp32 copies (or, with none, an fp32 wire) select the fp32 exchange."""
+    probe = stale[0] if len(stale) else wire
+    return probe is not None and probe.dtype == torch.float32
+
+
 def global_merge(params: torch.Tensor, stale: Sequence[torch.Tensor],
                  buckets: Sequence[Tuple[int, int, int]], wire: Optional[torch.Tensor] = None,
                  stream=None) -> torch.Tensor:
-    """Eq. (1) merge of the exchanged bf16 copies into params, in place."""
+    """Eq. (1) merge of the exchanged copies into params, in place: bf16 copies
+    (int16/bfloat16 tensors) use daso_global_merge, fp32 copies daso_global_merge_f32."""
     n = params.numel()
-    arr = _ptr_array(stale, _BF16, n, "stale")
+    f32 = _is_f32_exchange(stale, wire)
+    xt = _F32 if f32 else _BF16
+    arr = _ptr_array(stale, xt, n, "stale")
     bt = bucket_table(buckets)
-    _check(load().daso_global_merge(_ptr(params, _F32, n, "params"), arr, len(stale), bt, len(buckets),
-                                    _ptr(wire, _BF16, n, "wire"), n, _stream_handle(stream)),
-           "daso_global_merge")
+    fn = load().daso_global_merge_f32 if f32 else load().daso_global_merge
+    _check(fn(_ptr(params, _F32, n, "params"), arr, len(stale), bt, len(buckets), _ptr(wire, xt, n, "wire"), n,
+              _stream_handle(stream)), "daso_global_merge_f32" if f32 else "daso_global_merge")
     return params
 
 
@@ -186,8 +217,10 @@ class FusedStep:
                  flags: int = 0):
         n = params.numel()
         self._keep = (list(grads), params, momentum, list(stale), wire, grad_avg, stats)
+        f32 = _is_f32_exchange(stale, wire)
+        xt = _F32 if f32 else _BF16
         self._grads = _ptr_array(grads, _F32, n, "grads")
-        self._stale = _ptr_array(stale, _BF16, n, "stale")
+        self._stale = _ptr_array(stale, xt, n, "stale")
         self._buckets = bucket_table(buckets)
         if stats is not None:
             if not stats.is_cuda or stats.dtype != torch.float64 or tuple(stats.shape) != (len(buckets), 3) \
@@ -196,10 +229,15 @@ class FusedStep:
         a = daso_sync_args()
         a.n, a.g, a.P = n, len(grads), len(stale)
         a.grads = self._grads
-        a.stale = self._stale
+        if f32:
+            a.stale_f32 = self._stale
+            a.wire_f32 = _ptr(wire, xt, n, "wire")
+            flags |= DASO_EXCHANGE_F32
+        else:
+            a.stale = self._stale
+            a.wire = _ptr(wire, xt, n, "wire")
         a.params = _ptr(params, _F32, n, "params")
         a.momentum = _ptr(momentum, _F32, n, "momentum")
-        a.wire = _ptr(wire, _BF16, n, "wire")
         a.grad_avg = _ptr(grad_avg, _F32, n, "grad_avg")
         a.buckets = self._buckets
         a.nbuckets = len(buckets)

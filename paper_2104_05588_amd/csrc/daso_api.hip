@@ -194,6 +194,36 @@ extern "C" {
 
 int daso_abi_version(void) { return 100; }
 
+int32_t daso_plan_buckets(const int64_t* numels, int32_t ntensors, int64_t cap_elems, const int32_t* S_cycle,
+                          int32_t n_cycle, daso_bucket* out, int32_t out_cap) {
+  if (ntensors < 0 || cap_elems < 1 || n_cycle < 1 || S_cycle == nullptr || out_cap < 0) return DASO_EINVAL;
+  if (ntensors > 0 && numels == nullptr) return DASO_EINVAL;
+  if (out_cap > 0 && out == nullptr) return DASO_EINVAL;
+  for (int32_t c = 0; c < n_cycle; ++c)
+    if (S_cycle[c] < 0 || S_cycle[c] > kMaxS) return DASO_EINVAL;
+  int64_t end = 0;
+  for (int32_t i = 0; i < ntensors; ++i) {
+    if (numels[i] < 0) return DASO_EINVAL;
+    end += numels[i];
+  }
+  int32_t count = 0;
+  auto emit = [&](int64_t start, int64_t numel) {
+    if (count < out_cap) out[count] = daso_bucket{start, numel, S_cycle[count % n_cycle], 0};
+    ++count;
+  };
+  int64_t size = 0;
+  for (int32_t i = ntensors - 1; i >= 0; --i) {
+    size += numels[i];
+    if (size >= cap_elems) {
+      emit(end - size, size);
+      end -= size;
+      size = 0;
+    }
+  }
+  if (size > 0) emit(0, size);
+  return count;
+}
+
 const char* daso_status_string(int status) {
   switch (status) {
     case DASO_OK: return "DASO_OK: success";
@@ -240,23 +270,28 @@ int daso_pack_bf16(const float* src, uint16_t* wire, int64_t n, hipStream_t stre
   return run_groups(daso::kModePack, a, &whole, 1, nullptr, stream);
 }
 
-int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P, const daso_bucket* buckets,
-                      int32_t nbuckets, uint16_t* wire, int64_t n, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Eq. (1) merge with copies and wire of `esz` bytes per element (2: bf16, 4: fp32).
+int merge_impl(float* params, const void* const* stale, int32_t P, const daso_bucket* buckets, int32_t nbuckets,
+               void* wire, int64_t n, size_t esz, hipStream_t stream) {
   if (n < 0 || P < 0 || P > DASO_MAX_P) return DASO_EINVAL;
   int rc = check_out(params);
   if (rc != DASO_OK) return rc;
-  if ((rc = check_ptr_table(reinterpret_cast<const void* const*>(stale), P)) != DASO_OK) return rc;
+  if ((rc = check_ptr_table(stale, P)) != DASO_OK) return rc;
   if (wire && !aligned16(wire)) return DASO_EALIGN;
   if (n == 0) return DASO_OK;
   if ((rc = check_buckets(buckets, nbuckets, n)) != DASO_OK) return rc;
   const Span sx = span_of(params, n, 4);
   for (int32_t i = 0; i < P; ++i)
-    if (overlaps(sx, span_of(stale[i], n, 2))) return DASO_EALIAS;
+    if (overlaps(sx, span_of(stale[i], n, esz))) return DASO_EALIAS;
   if (wire) {
-    const Span sw = span_of(wire, n, 2);
+    const Span sw = span_of(wire, n, esz);
     if (overlaps(sw, sx)) return DASO_EALIAS;
     for (int32_t i = 0; i < P; ++i)
-      if (overlaps(sw, span_of(stale[i], n, 2))) return DASO_EALIAS;
+      if (overlaps(sw, span_of(stale[i], n, esz))) return DASO_EALIAS;
   }
 
   StepArgs a;
@@ -265,22 +300,45 @@ int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P, co
   a.P = P;
   a.x = params;
   a.wire = wire;
+  a.xf32 = esz == 4 ? 1 : 0;
   return run_groups(daso::kModeMerge, a, buckets, nbuckets, nullptr, stream);
+}
+
+}  // namespace
+
+extern "C" {
+
+int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P, const daso_bucket* buckets,
+                      int32_t nbuckets, uint16_t* wire, int64_t n, hipStream_t stream) {
+  return merge_impl(params, reinterpret_cast<const void* const*>(stale), P, buckets, nbuckets, wire, n, 2, stream);
+}
+
+int daso_global_merge_f32(float* params, const float* const* stale, int32_t P, const daso_bucket* buckets,
+                          int32_t nbuckets, float* wire, int64_t n, hipStream_t stream) {
+  return merge_impl(params, reinterpret_cast<const void* const*>(stale), P, buckets, nbuckets, wire, n, 4, stream);
 }
 
 int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
   if (args == nullptr) return DASO_EINVAL;
   const daso_sync_args& s = *args;
   if (s.n < 0 || s.g < 1 || s.g > DASO_MAX_G || s.P < 0 || s.P > DASO_MAX_P) return DASO_EINVAL;
+  if ((s.flags & ~(DASO_PACK_PRE_MERGE | DASO_EXCHANGE_F32)) != 0) return DASO_EINVAL;
+  const bool xf32 = (s.flags & DASO_EXCHANGE_F32) != 0;
+  // the exchanged copies and the wire, in the exchange type
+  const void* const* stale = xf32 ? reinterpret_cast<const void* const*>(s.stale_f32)
+                                  : reinterpret_cast<const void* const*>(s.stale);
+  void* wire = xf32 ? static_cast<void*>(s.wire_f32) : static_cast<void*>(s.wire);
+  const size_t esz = xf32 ? 4 : 2;
+  if (xf32 ? (s.stale != nullptr || s.wire != nullptr) : (s.stale_f32 != nullptr || s.wire_f32 != nullptr))
+    return DASO_EINVAL;
   int rc = check_ptr_table(reinterpret_cast<const void* const*>(s.grads), s.g);
   if (rc != DASO_OK) return rc;
-  if ((rc = check_ptr_table(reinterpret_cast<const void* const*>(s.stale), s.P)) != DASO_OK) return rc;
+  if ((rc = check_ptr_table(stale, s.P)) != DASO_OK) return rc;
   if ((rc = check_out(s.params)) != DASO_OK) return rc;
   if ((rc = check_out(s.momentum)) != DASO_OK) return rc;
-  if (s.wire && !aligned16(s.wire)) return DASO_EALIGN;
+  if (wire && !aligned16(wire)) return DASO_EALIGN;
   if (s.grad_avg && !aligned16(s.grad_avg)) return DASO_EALIGN;
   if (s.stats && (reinterpret_cast<uintptr_t>(s.stats) & 7u) != 0) return DASO_EALIGN;
-  if ((s.flags & ~DASO_PACK_PRE_MERGE) != 0) return DASO_EINVAL;
   if (s.n == 0) return DASO_OK;
   if ((rc = check_buckets(s.buckets, s.nbuckets, s.n)) != DASO_OK) return rc;
 
@@ -289,9 +347,9 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
   const Span sm = span_of(s.momentum, s.n, 4);
   std::vector<Span> inputs;
   for (int32_t r = 0; r < s.g; ++r) inputs.push_back(span_of(s.grads[r], s.n, 4));
-  for (int32_t i = 0; i < s.P; ++i) inputs.push_back(span_of(s.stale[i], s.n, 2));
+  for (int32_t i = 0; i < s.P; ++i) inputs.push_back(span_of(stale[i], s.n, esz));
   std::vector<Span> outs = {sx, sm};
-  if (s.wire) outs.push_back(span_of(s.wire, s.n, 2));
+  if (wire) outs.push_back(span_of(wire, s.n, esz));
   if (s.stats) outs.push_back(span_of(s.stats, s.nbuckets, sizeof(daso_bucket_stats)));
   for (size_t i = 0; i < outs.size(); ++i) {
     for (size_t j = i + 1; j < outs.size(); ++j)
@@ -312,12 +370,13 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
   StepArgs a;
   memset(&a, 0, sizeof(a));
   for (int32_t r = 0; r < s.g; ++r) a.grads[r] = s.grads[r];
-  for (int32_t i = 0; i < s.P; ++i) a.stale[i] = s.stale[i];
+  for (int32_t i = 0; i < s.P; ++i) a.stale[i] = stale[i];
   a.g = s.g;
   a.P = s.P;
   a.x = s.params;
   a.m = s.momentum;
-  a.wire = s.wire;
+  a.wire = wire;
+  a.xf32 = xf32 ? 1 : 0;
   a.gavg = s.grad_avg;
   a.lr = s.lr;
   a.mu = s.mu;

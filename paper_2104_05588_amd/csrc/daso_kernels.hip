@@ -107,6 +107,35 @@ __device__ __forceinline__ f32x4 widen4(u32x2 h) {
   return r;
 }
 
+// The exchanged copies and the wire are bf16 (XF = false) or fp32 (XF = true,
+// the non-blocking exchange of Section 3, which is not cast).
+template <bool XF>
+struct XType {
+  using T = u32x2;
+};
+template <>
+struct XType<true> {
+  using T = f32x4;
+};
+
+template <bool XF, bool FULL>
+__device__ __forceinline__ typename XType<XF>::T load_x(const void* p, int64_t e0, unsigned mask) {
+  if constexpr (XF) return load_f32<FULL, true>(static_cast<const float*>(p), e0, mask);
+  else return load_bf16<FULL>(static_cast<const uint16_t*>(p), e0, mask);
+}
+
+template <bool XF>
+__device__ __forceinline__ f32x4 received(typename XType<XF>::T v) {
+  if constexpr (XF) return v;
+  else return widen4(v);
+}
+
+template <bool XF, bool FULL>
+__device__ __forceinline__ void store_wire(void* p, int64_t e0, unsigned mask, f32x4 v) {
+  if constexpr (XF) store_f32<FULL, true>(static_cast<float*>(p), e0, mask, v);
+  else store_bf16<FULL>(static_cast<uint16_t*>(p), e0, mask, pack4(v));
+}
+
 // Division by a per-bucket or per-call constant.  For a power of two the
 // product with its (exact) reciprocal equals the correctly rounded quotient.
 struct Divisor {
@@ -191,12 +220,12 @@ __device__ __forceinline__ AccT<CountT> block_sum(AccT<CountT> v) {
 }
 
 // ----------------------------------------------------------- one 4-vector
-template <int MODE, int G, int PP, bool FULL, bool STATS>
+template <int MODE, int G, int PP, bool FULL, bool STATS, bool XF>
 __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned mask, float two_s,
                                          const Divisor& qg, const Divisor& qm, Acc& acc) {
   if constexpr (MODE == kModePack) {
     const f32x4 v = load_f32<FULL, true>(a.src, e0, mask);
-    store_bf16<FULL>(a.wire, e0, mask, pack4(v));
+    store_wire<false, FULL>(a.wire, e0, mask, v);
     return;
   }
   const int g = (G > 0) ? G : a.g;
@@ -227,13 +256,13 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
   if (P > 0) {
     f32x4 acc4 = two_s * xl;
 #pragma unroll
-    for (int i = 0; i < P; ++i) acc4 = acc4 + widen4(load_bf16<FULL>(a.stale[i], e0, mask));
+    for (int i = 0; i < P; ++i) acc4 = acc4 + received<XF>(load_x<XF, FULL>(a.stale[i], e0, mask));
     xn = divide(acc4, qm);
   }
   store_f32<FULL, false>(a.x, e0, mask, xn);
   if (a.wire) {
     const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
-    store_bf16<FULL>(a.wire, e0, mask, pack4(pre ? xl : xn));
+    store_wire<XF, FULL>(a.wire, e0, mask, pre ? xl : xn);
   }
   if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
 }
@@ -243,34 +272,35 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
 // wavefront keeps every stream of several vectors in flight at once (the
 // compiler cannot move later loads above earlier stores by itself: it cannot
 // prove that the streams do not overlap).
-template <int MODE, int G, int PP>
+template <int MODE, int G, int PP, bool XF>
 struct VecIn {
   static constexpr int kG = (MODE == kModeAvg || MODE == kModeFused) ? G : 0;
   static constexpr int kP = (MODE == kModeMerge || MODE == kModeFused) ? PP : 0;
   f32x4 g[kG > 0 ? kG : 1];
   f32x4 x;  // params (merge, fused) or the source (pack)
   f32x4 m;  // momentum (fused)
-  u32x2 s[kP > 0 ? kP : 1];
+  typename XType<XF>::T s[kP > 0 ? kP : 1];
 };
 
-template <int MODE, int G, int PP, bool FULL>
-__device__ __forceinline__ void load_in(const StepArgs& a, int64_t e0, unsigned mask, VecIn<MODE, G, PP>& v) {
-  using V = VecIn<MODE, G, PP>;
+template <int MODE, int G, int PP, bool XF, bool FULL>
+__device__ __forceinline__ void load_in(const StepArgs& a, int64_t e0, unsigned mask, VecIn<MODE, G, PP, XF>& v) {
+  using V = VecIn<MODE, G, PP, XF>;
 #pragma unroll
   for (int r = 0; r < V::kG; ++r) v.g[r] = load_f32<FULL, true>(a.grads[r], e0, mask);
   if constexpr (MODE == kModePack) v.x = load_f32<FULL, true>(a.src, e0, mask);
   if constexpr (MODE == kModeMerge || MODE == kModeFused) v.x = load_f32<FULL, kNtParams>(a.x, e0, mask);
   if constexpr (MODE == kModeFused) v.m = load_f32<FULL, kNtParams>(a.m, e0, mask);
 #pragma unroll
-  for (int i = 0; i < V::kP; ++i) v.s[i] = load_bf16<FULL>(a.stale[i], e0, mask);
+  for (int i = 0; i < V::kP; ++i) v.s[i] = load_x<XF, FULL>(a.stale[i], e0, mask);
 }
 
-template <int MODE, int G, int PP, bool FULL, bool STATS>
-__device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned mask, const VecIn<MODE, G, PP>& v,
-                                       float two_s, const Divisor& qg, const Divisor& qm, Acc& acc) {
-  using V = VecIn<MODE, G, PP>;
+template <int MODE, int G, int PP, bool XF, bool FULL, bool STATS>
+__device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned mask,
+                                       const VecIn<MODE, G, PP, XF>& v, float two_s, const Divisor& qg,
+                                       const Divisor& qm, Acc& acc) {
+  using V = VecIn<MODE, G, PP, XF>;
   if constexpr (MODE == kModePack) {
-    store_bf16<FULL>(a.wire, e0, mask, pack4(v.x));
+    store_wire<false, FULL>(a.wire, e0, mask, v.x);
     return;
   }
   f32x4 gbar = {0.f, 0.f, 0.f, 0.f};
@@ -297,13 +327,13 @@ __device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned m
   if constexpr (V::kP > 0) {
     f32x4 acc4 = two_s * xl;
 #pragma unroll
-    for (int i = 0; i < V::kP; ++i) acc4 = acc4 + widen4(v.s[i]);
+    for (int i = 0; i < V::kP; ++i) acc4 = acc4 + received<XF>(v.s[i]);
     xn = divide(acc4, qm);
   }
   store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
   if (a.wire) {
     const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
-    store_bf16<FULL>(a.wire, e0, mask, pack4(pre ? xl : xn));
+    store_wire<XF, FULL>(a.wire, e0, mask, pre ? xl : xn);
   }
   if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
 }
@@ -319,30 +349,32 @@ constexpr bool batched() {
 
 // Vectors per batch: as many as DASO_BATCH allows while the batch's input
 // registers stay within about 48 VGPRs per vector.
-template <int MODE, int G, int PP>
+template <int MODE, int G, int PP, bool XF>
 constexpr int batch_of() {
-  using V = VecIn<MODE, G, PP>;
-  constexpr int regs = 4 * V::kG + 2 * V::kP + ((MODE == kModeFused) ? 8 : 4);
+  using V = VecIn<MODE, G, PP, XF>;
+  constexpr int regs = 4 * V::kG + (XF ? 4 : 2) * V::kP + ((MODE == kModeFused) ? 8 : 4);
   return regs <= 48 ? kBatch : 1;
 }
 
 // ------------------------------------------------------------------- tiles
-template <int MODE, int G, int PP, bool STATS>
+template <int MODE, int G, int PP, bool STATS, bool XF>
 __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64_t tlo, int64_t thi, float two_s,
                                          const Divisor& qg, const Divisor& qm, Acc& acc) {
   constexpr bool kBatched = batched<MODE, G, PP>();
   const int64_t t0 = abase + int64_t(threadIdx.x) * kVec;
   if constexpr (kBatched) {
     if (tlo == abase && thi == abase + kTile) {
-      constexpr int B = batch_of<MODE, G, PP>();
+      constexpr int B = batch_of<MODE, G, PP, XF>();
       static_assert(kIters % B == 0, "batch must divide the iterations");
       for (int it = 0; it < kIters; it += B) {
-        VecIn<MODE, G, PP> v[B];
-#pragma unroll
-        for (int b = 0; b < B; ++b) load_in<MODE, G, PP, true>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b]);
+        VecIn<MODE, G, PP, XF> v[B];
 #pragma unroll
         for (int b = 0; b < B; ++b)
-          finish<MODE, G, PP, true, STATS>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm, acc);
+          load_in<MODE, G, PP, XF, true>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b]);
+#pragma unroll
+        for (int b = 0; b < B; ++b)
+          finish<MODE, G, PP, XF, true, STATS>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm,
+                                               acc);
       }
       return;
     }
@@ -359,17 +391,17 @@ __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64
         if (e0 + k >= tlo && e0 + k < thi) mask |= 1u << k;
     }
     if constexpr (kBatched) {
-      VecIn<MODE, G, PP> v;
+      VecIn<MODE, G, PP, XF> v;
       if (full) {
-        load_in<MODE, G, PP, true>(a, e0, mask, v);
-        finish<MODE, G, PP, true, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
+        load_in<MODE, G, PP, XF, true>(a, e0, mask, v);
+        finish<MODE, G, PP, XF, true, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
       } else {
-        load_in<MODE, G, PP, false>(a, e0, mask, v);
-        finish<MODE, G, PP, false, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
+        load_in<MODE, G, PP, XF, false>(a, e0, mask, v);
+        finish<MODE, G, PP, XF, false, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
       }
     } else {
-      if (full) step_vec<MODE, G, PP, true, STATS>(a, e0, mask, two_s, qg, qm, acc);
-      else step_vec<MODE, G, PP, false, STATS>(a, e0, mask, two_s, qg, qm, acc);
+      if (full) step_vec<MODE, G, PP, true, STATS, XF>(a, e0, mask, two_s, qg, qm, acc);
+      else step_vec<MODE, G, PP, false, STATS, XF>(a, e0, mask, two_s, qg, qm, acc);
     }
   }
 }
@@ -385,7 +417,7 @@ __device__ __forceinline__ int xcd_ordered(int w, int grid) {
 
 // Workgroups take tiles w, w + gridDim.x, ...; the grid is either one workgroup
 // per tile or a few workgroups per compute unit.
-template <int MODE, int G, int PP, bool STATS>
+template <int MODE, int G, int PP, bool STATS, bool XF>
 __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   const int P = (PP >= 0) ? PP : a.P;
   const Divisor qg = make_divisor((G > 0) ? G : a.g);
@@ -407,7 +439,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
     const Divisor qm = make_divisor(2 * bk.S + P);
 
     Acc acc = {0.0, 0.0, 0u};
-    run_tile<MODE, G, PP, STATS>(a, abase, tlo, thi, two_s, qg, qm, acc);
+    run_tile<MODE, G, PP, STATS, XF>(a, abase, tlo, thi, two_s, qg, qm, acc);
     if constexpr (STATS && MODE == kModeFused) {
       const Acc t = block_sum(acc);
       if (threadIdx.x == 0) {
@@ -444,9 +476,9 @@ __global__ __launch_bounds__(kBlock) void stats_kernel(const StepArgs a) {
   }
 }
 
-template <int MODE, int G, int PP, bool STATS>
+template <int MODE, int G, int PP, bool STATS, bool XF = false>
 hipError_t launch(const StepArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS>), dim3(grid), dim3(kBlock), 0, stream, a);
+  hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS, XF>), dim3(grid), dim3(kBlock), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !STATS) return e;
   hipLaunchKernelGGL(stats_kernel, dim3(a.nb), dim3(kBlock), 0, stream, a);
@@ -457,6 +489,10 @@ template <bool STATS>
 hipError_t launch_fused(const StepArgs& a, int grid, hipStream_t stream) {
   // Fully unrolled instances for common (g, P); any other pair takes the
   // runtime-count instance, which computes the same bits.
+  if (a.xf32) {
+    if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS, true>(a, grid, stream);
+    return launch<kModeFused, 0, -1, STATS, true>(a, grid, stream);
+  }
   if (a.g == 4 && a.P == 2) return launch<kModeFused, 4, 2, STATS>(a, grid, stream);
   if (a.g == 4 && a.P == 4) return launch<kModeFused, 4, 4, STATS>(a, grid, stream);
   if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS>(a, grid, stream);
@@ -480,6 +516,10 @@ hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, int grid, 
     case kModePack:
       return launch<kModePack, 0, -1, false>(a, grid, stream);
     case kModeMerge:
+      if (a.xf32) {
+        if (a.P == 8) return launch<kModeMerge, 0, 8, false, true>(a, grid, stream);
+        return launch<kModeMerge, 0, -1, false, true>(a, grid, stream);
+      }
       switch (a.P) {
         case 0: return launch<kModeMerge, 0, 0, false>(a, grid, stream);
         case 2: return launch<kModeMerge, 0, 2, false>(a, grid, stream);

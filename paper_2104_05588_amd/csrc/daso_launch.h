@@ -61,11 +61,11 @@ struct TilePartial {
 // Kernel arguments, passed by value (about 2.7 KB).
 struct StepArgs {
   const float* grads[DASO_MAX_G];
-  const uint16_t* stale[DASO_MAX_P];
+  const void* stale[DASO_MAX_P];  // bf16 patterns, or fp32 when xf32
   const float* src;      // pack: source fp32
   float* x;              // params (merge/fused, in place)
   float* m;              // momentum (fused, in place)
-  uint16_t* wire;        // packed output or nullptr
+  void* wire;            // packed output (bf16, or fp32 when xf32) or nullptr
   float* gavg;           // local average output or nullptr
   TilePartial* partials; // per-tile partials (stats only)
   daso_bucket_stats* stats;  // per-bucket outputs (stats only), already offset to this launch
@@ -78,6 +78,7 @@ struct StepArgs {
   int32_t nb;            // buckets in this launch
   int32_t ntiles;        // tiles in this launch
   int32_t xcd_order;     // nonzero: renumber workgroups XCD-contiguously
+  int32_t xf32;          // nonzero: fp32 exchange (stale copies and wire are fp32)
   TileBucket b[kLaunchBuckets];
 };
 

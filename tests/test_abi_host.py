@@ -52,10 +52,30 @@ def test_status_strings_and_version(lib):
     assert "unknown" in L.status_string(-99)
 
 
-def test_struct_layouts_match_header():
-    assert ctypes.sizeof(L.daso_bucket) == 24
-    assert ctypes.sizeof(L.daso_bucket_stats) == 24
-    assert L.daso_sync_args.stats.offset == ctypes.sizeof(L.daso_sync_args) - 8
+def test_struct_layouts_match_header(tmp_path):
+    """Field offsets and sizes of the binding's ctypes structs equal what a C
+    compiler makes of include/daso.h."""
+    import subprocess
+    fields = {"daso_bucket": [f[0] for f in L.daso_bucket._fields_],
+              "daso_bucket_stats": [f[0] for f in L.daso_bucket_stats._fields_],
+              "daso_sync_args": [f[0] for f in L.daso_sync_args._fields_]}
+    src = ["#include <stdio.h>", "#include <stddef.h>", '#include "daso.h"', "int main(void) {"]
+    for st, names in fields.items():
+        src.append(f'  printf("{st} size %zu\\n", sizeof({st}));')
+        for f in names:
+            src.append(f'  printf("{st} {f} %zu\\n", offsetof({st}, {f}));')
+    src.append("  return 0; }")
+    c = tmp_path / "layout.c"
+    c.write_text("\n".join(src) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+                    str(c), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    for line in filter(None, out):
+        st, f, v = line.split()
+        cls = getattr(L, st)
+        want = ctypes.sizeof(cls) if f == "size" else getattr(cls, f).offset
+        assert int(v) == want, (st, f, int(v), want)
 
 
 # ------------------------------------------------------------- validation
@@ -163,3 +183,57 @@ def test_fused_rejects(lib):
     assert rc(stats=A + 22 * MB) == L.DASO_EALIAS                # stats on the wire
     assert rc(nbuckets=0) == L.DASO_EINVAL
     assert rc(n=0) == L.DASO_OK
+    # fp32 exchange: the copies and the wire move to stale_f32 / wire_f32
+    st32 = ptrs(A + 10 * MB, A + 14 * MB)
+    assert rc(flags=L.DASO_EXCHANGE_F32) == L.DASO_EINVAL                        # stale still set
+    assert rc(stale_f32=st32) == L.DASO_EINVAL                                   # without the flag
+    assert rc(flags=L.DASO_EXCHANGE_F32, stale=None, wire=None,
+              stale_f32=st32, wire_f32=A + 10 * MB + 2000) == L.DASO_EALIAS     # wire inside copy 0 (4 B/elem)
+    assert rc(flags=L.DASO_EXCHANGE_F32, stale=None, wire=None,
+              stale_f32=st32, wire_f32=A + 30 * MB + 8) == L.DASO_EALIGN
+    assert rc(flags=L.DASO_EXCHANGE_F32, stale=None, wire=None, n=0, stale_f32=st32) == L.DASO_OK
+
+
+def test_global_merge_f32_rejects(lib):
+    _no_gpu()
+    f, n = lib.daso_global_merge_f32, 1000
+    st = ptrs(A + MB, A + 2 * MB)
+    ok_b = L.bucket_table([(0, 1000, 1)])
+    assert f(A, ptrs(A + 2048, A + 2 * MB), 2, ok_b, 1, None, n, None) == L.DASO_EALIAS   # 4 B/elem overlap
+    assert f(A, st, 2, ok_b, 1, A + MB + 3200, n, None) == L.DASO_EALIAS               # wire inside copy 0
+    assert f(A, st, 2, L.bucket_table([(0, 999, 1)]), 1, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 2, ok_b, 1, None, 0, None) == L.DASO_OK
+
+
+# ----------------------------------------------------------- bucket plan
+def test_plan_buckets_matches_the_workload_recipes(lib):
+    """The library's layout planner reproduces the bucket tables of every
+    workload (whose counts are pinned in test_workloads.py)."""
+    from workloads import recipes as R
+    for w in R.all_workloads():
+        if w.name == "tiny":
+            continue  # a single explicit bucket, not planned
+        got = L.plan_buckets(list(w.numels), R.BUCKET_CAP_ELEMS, w.S_cycle)
+        assert got == [(b.start, b.numel, b.S) for b in w.buckets], w.name
+
+
+def test_plan_buckets_random_and_edges(lib):
+    import numpy as np
+    from workloads import recipes as R
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        nt = int(rng.integers(0, 40))
+        numels = rng.integers(0, 1000, nt).tolist()
+        cap = int(rng.integers(1, 3000))
+        cyc = rng.integers(0, 9, int(rng.integers(1, 5))).tolist()
+        want = [(s, k, cyc[b % len(cyc)]) for b, (s, k) in enumerate(R.plan_buckets(numels, cap))]
+        assert L.plan_buckets(numels, cap, cyc) == want
+    assert L.plan_buckets([], 10) == []
+    assert L.plan_buckets([5, 3, 4, 10, 1], 8, (2,)) == [(12, 11, 2), (0, 12, 2)]
+    f = lib.daso_plan_buckets
+    i64 = (ctypes.c_int64 * 2)(4, -1)
+    one = (ctypes.c_int32 * 1)(1)
+    assert f(i64, 2, 10, one, 1, None, 0) == L.DASO_EINVAL
+    assert f((ctypes.c_int64 * 1)(4), 1, 0, one, 1, None, 0) == L.DASO_EINVAL
+    assert f((ctypes.c_int64 * 1)(4), 1, 10, (ctypes.c_int32 * 1)(-2), 1, None, 0) == L.DASO_EINVAL
+    assert f((ctypes.c_int64 * 1)(4), 1, 10, one, 1, None, 1) == L.DASO_EINVAL

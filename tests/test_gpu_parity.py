@@ -119,20 +119,20 @@ def random_inputs(rng, n, g, P, specials=False):
     return {"params": x, "momentum": m, "grads": grads, "stale": stale}
 
 
-def run_fused(inp, buckets, lr=0.1, mu=0.9, wd=0.0, flags=0, wire=True, gavg="none", stats=True):
+def run_fused(inp, buckets, lr=0.1, mu=0.9, wd=0.0, flags=0, wire=True, gavg="none", stats=True, f32=False):
     n = inp["params"].shape[0]
     grads = [dev_f32(a) for a in inp["grads"]]
-    stale = [dev_bf16(a) for a in inp["stale"]]
+    stale = [(dev_f32 if f32 else dev_bf16)(a) for a in inp["stale"]]
     x = dev_f32(inp["params"])
     m = dev_f32(inp["momentum"])
-    w = torch.empty(n, dtype=torch.int16, device="cuda") if wire else None
+    w = torch.empty(n, dtype=torch.float32 if f32 else torch.int16, device="cuda") if wire else None
     ga = grads[0] if gavg == "alias" else (torch.empty(n, dtype=torch.float32, device="cuda")
                                            if gavg == "new" else None)
     st = daso.new_stats(len(buckets)) if stats else None
     daso.fused_sync_step(grads, x, m, stale, buckets, lr, mu, wd, w, ga, st, flags)
     torch.cuda.synchronize()
     return {"params": host_f32(x), "momentum": host_f32(m),
-            "wire": host_u16(w) if wire else None,
+            "wire": (host_f32(w) if f32 else host_u16(w)) if wire else None,
             "grad_avg": host_f32(ga) if ga is not None else None,
             "stats": daso.decode_stats(st) if stats else None}
 
@@ -141,7 +141,7 @@ def compare_fused(got, want, what, wire=True, gavg=False, stats=True):
     check_f32(got["params"], want["params"], what + " params")
     check_f32(got["momentum"], want["momentum"], what + " momentum")
     if wire:
-        check_u16(got["wire"], want["wire"], what + " wire")
+        (check_f32 if want["wire"].dtype == F32 else check_u16)(got["wire"], want["wire"], what + " wire")
     if gavg:
         check_f32(got["grad_avg"], want["grad_avg"], what + " grad_avg")
     if stats:
@@ -413,3 +413,44 @@ def test_fused_gpt_medium_full_size_sampled():
         assert abs(got[b][0] - gsq) <= 1e-9 * gsq, (b, got[b], gsq)
         assert abs(got[b][1] - dsq) <= 1e-9 * dsq, (b, got[b], dsq)
         assert got[b][2] == 0
+
+
+# ------------------------------------------------------------ fp32 exchange
+@pytest.mark.parametrize("P", [0, 3, 8, 20])
+def test_global_merge_f32(P):
+    rng = np.random.default_rng(400 + P)
+    for n in (5, 4097, 200_003):
+        bks = random_buckets(rng, n, 4)
+        announce("global_merge_f32 P=", P, "n=", n)
+        x = (rng.standard_normal(n) * 0.02).astype(F32)
+        st = [(x + (rng.standard_normal(n) * 1e-4).astype(F32)).astype(F32) for _ in range(P)]
+        want, wire_want = O.global_merge(x, st, bks, pack=True, exchange="f32")
+        xd = dev_f32(x)
+        wd = torch.empty(n, dtype=torch.float32, device="cuda")
+        daso.global_merge(xd, [dev_f32(a) for a in st], bks, wd)
+        torch.cuda.synchronize()
+        check_f32(host_f32(xd), want, f"merge_f32 P={P} n={n}")
+        check_f32(host_f32(wd), wire_want, f"merge_f32 wire P={P} n={n}")
+
+
+F32X_CASES = [
+    # (seed, n, g, P, nbuckets, wd, flags)
+    (61, 50_001, 4, 8, 3, 0.0, 0),
+    (62, 33_333, 3, 5, 4, 1e-4, daso.DASO_PACK_PRE_MERGE),
+    (63, 4097, 8, 32, 2, 0.0, 0),
+    (64, 262_144, 4, 8, 1, 0.0, daso.DASO_PACK_PRE_MERGE),
+]
+
+
+@pytest.mark.parametrize("case", F32X_CASES, ids=[f"s{c[0]}_n{c[1]}_g{c[2]}_P{c[3]}" for c in F32X_CASES])
+def test_fused_f32_exchange(case):
+    seed, n, g, P, nb, wd, flags = case
+    rng = np.random.default_rng(seed)
+    bks = random_buckets(rng, n, nb)
+    inp = random_inputs(rng, n, g, 0, specials=(seed == 62))
+    inp["stale"] = [(inp["params"] + (rng.standard_normal(n) * 1e-4).astype(F32)).astype(F32) for _ in range(P)]
+    announce("fused f32 exchange", case)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9, wd, flags,
+                             exchange="f32")
+    got = run_fused(inp, bks, wd=wd, flags=flags, gavg="new", f32=True)
+    compare_fused(got, want, f"fused f32 {case}", gavg=True)

@@ -389,3 +389,51 @@ def test_bucket_validation():
     for bad in ([(0, 50, 1)], [(0, 60, 1), (50, 50, 1)], [(0, 100, -1)], [(1, 99, 1)]):
         with pytest.raises(ValueError):
             O.fused_sync_step(grads, x, m, stale, bad, 0.1, 0.9)
+
+
+# ---------------------------------------------------------- fp32 exchange
+def test_merge_f32_small_integers_match_exact_rational_eq1():
+    """fp32 exchange: integers up to 2^20 are exact binary32 values whose sums
+    stay exact, so only the final division rounds (exact rational Eq. (1))."""
+    rng = np.random.default_rng(50)
+    for S in range(0, 5):
+        for P in range(1, 7):
+            xl = rng.integers(-(1 << 20), 1 << 20, 16).astype(F32)
+            st = [rng.integers(-(1 << 20), 1 << 20, 16).astype(F32) for _ in range(P)]
+            got = O.merge_eq1(xl, st, S)
+            for j in range(16):
+                num = 2 * S * Fraction(int(xl[j])) + sum(Fraction(int(s[j])) for s in st)
+                assert got[j] == frac_to_f32(num / (2 * S + P)), (S, P, j)
+
+
+def test_f32_exchange_equals_bf16_exchange_on_bf16_values():
+    """Copies that are exactly bf16 values merge to the same bits whichever way
+    they travel; the fp32 wire then holds x' itself."""
+    grads, x, m, stale, buckets = _small_case(n=3001, seed=51)
+    st32 = [O.bf16_widen(s) for s in stale]
+    a = O.fused_sync_step(grads, x, m, stale, buckets, 0.1, 0.9)
+    b = O.fused_sync_step(grads, x, m, st32, buckets, 0.1, 0.9, exchange="f32")
+    assert np.array_equal(f32_bits(a["params"]), f32_bits(b["params"]))
+    assert np.array_equal(f32_bits(b["wire"]), f32_bits(b["params"]))
+    pre = O.fused_sync_step(grads, x, m, st32, buckets, 0.1, 0.9, flags=O.PACK_PRE_MERGE, exchange="f32")
+    assert np.array_equal(f32_bits(pre["wire"]), f32_bits(pre["x_local"]))
+    with pytest.raises(TypeError):
+        O.fused_sync_step(grads, x, m, stale, buckets, 0.1, 0.9, exchange="f32")
+
+
+def test_merge_f32_gradient_form_appendix():
+    """The appendix's gradient form, with fp32 copies (no bf16 rounding)."""
+    rng = np.random.default_rng(52)
+    n, eta = 4000, 0.1
+    for S, P in ((1, 2), (4, 8), (8, 32), (3, 7)):
+        xt = (rng.standard_normal(n) * 0.02).astype(F32)
+        Gl = [(rng.standard_normal(n) * 1e-3).astype(F32) for _ in range(S)]
+        xl = xt.copy()
+        for G in Gl:
+            xl = xl - F32(eta) * G
+        st = [(xt - F32(eta) * (rng.standard_normal(n) * 1e-3).astype(F32)).astype(F32) for _ in range(P)]
+        Gp = [(xt.astype(np.float64) - s.astype(np.float64)) / eta for s in st]
+        GlS = (xt.astype(np.float64) - xl.astype(np.float64)) / eta
+        want = xt.astype(np.float64) - eta / (2 * S + P) * (2 * S * GlS + np.sum(np.stack(Gp), axis=0))
+        got = O.merge_eq1(xl, st, S).astype(np.float64)
+        assert np.max(np.abs(got - want)) <= (P + 3) * 2.0 ** -24 * 0.1, (S, P)
