@@ -174,6 +174,76 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
 int32_t daso_plan_buckets(const int64_t* numels, int32_t ntensors, int64_t cap_elems,
                           const int32_t* S_cycle, int32_t n_cycle, daso_bucket* out, int32_t out_cap);
 
+/* ------------------------------------------------------------------------
+ * Phase and schedule controller (host only; Section 3).  Training runs for a
+ * fixed number of epochs in three phases: warm-up and cool-down epochs use
+ * blocking global synchronisation after every batch; the cycling phase in
+ * between uses non-blocking synchronisation: a global exchange starts every B
+ * batches and its copies are merged W batches later with S = W in Eq. (1).  B is
+ * set by hand; W starts at B/4.  Each time the training loss plateaus, B and W
+ * halve (down to 1); once both are 1 and the loss plateaus again they return to
+ * their initial values.  The role of global synchronisation rotates between the
+ * groups (the GPUs with the same local rank on every node): exchange k is done
+ * by group k mod group_count, whose member then broadcasts the merged state to
+ * the other GPUs of its node.
+ *
+ * Readings where the paper is silent: a plateau is `patience` consecutive
+ * cycling epochs whose loss does not fall below best - plateau_rel_tol * |best|
+ * (best: the last loss that did); after a change of B and W the count restarts;
+ * the new values apply from the next epoch; in cycling, an exchange is started
+ * only if its copies land no later than the last cycling batch and not in a
+ * batch where another exchange's copies land; blocking exchanges also rotate
+ * between groups; the first exchange of the cycling phase starts after its
+ * B-th batch.
+ */
+#define DASO_PHASE_WARMUP 0
+#define DASO_PHASE_CYCLING 1
+#define DASO_PHASE_COOLDOWN 2
+
+#define DASO_ACT_SEND 1u       /* after this batch's step, start a non-blocking exchange */
+#define DASO_ACT_MERGE 2u      /* copies sent S batches ago arrived: merge them with S */
+#define DASO_ACT_BLOCKING 4u   /* blocking exchange and plain average (S = 0) after this batch */
+#define DASO_ACT_RECV_BCAST 8u /* take the merged state broadcast by this node's group member */
+
+typedef struct daso_schedule_config {
+  int32_t total_epochs;      /* >= 1 */
+  int32_t warmup_epochs;     /* >= 0 */
+  int32_t cooldown_epochs;   /* >= 0; warmup_epochs + cooldown_epochs <= total_epochs */
+  int32_t batches_per_epoch; /* >= 1 */
+  int32_t B_init;            /* >= 1: batches between exchanges when cycling starts */
+  int32_t W_init;            /* 1..B_init, or 0 for max(1, B_init / 4) */
+  int32_t group_count;       /* >= 1: GPUs per node */
+  int32_t local_rank;        /* 0..group_count-1: this GPU's group */
+  int32_t patience;          /* >= 1 */
+  double plateau_rel_tol;    /* >= 0 */
+} daso_schedule_config;
+
+/* What this GPU does around one batch. */
+typedef struct daso_batch_plan {
+  int64_t step;        /* batch index since the start of training */
+  int32_t epoch;
+  int32_t batch;       /* index within the epoch */
+  int32_t phase;       /* DASO_PHASE_* */
+  int32_t B;           /* current exchange period (cycling) */
+  int32_t W;           /* current wait (cycling) */
+  uint32_t actions;    /* DASO_ACT_* bits for this GPU; 0: local synchronisation and step only */
+  int32_t S;           /* staleness for DASO_ACT_MERGE (or 0 with DASO_ACT_BLOCKING), else -1 */
+  int32_t sync_group;  /* group whose exchange starts (or blocks) after this batch, or -1 */
+  int32_t merge_group; /* group that merges arrived copies after this batch, or -1 */
+} daso_batch_plan;
+
+typedef struct daso_schedule daso_schedule; /* opaque, owned by the caller through create/destroy */
+
+/* Create a controller; DASO_EINVAL for an invalid configuration. */
+int daso_schedule_create(const daso_schedule_config* cfg, daso_schedule** out);
+/* Plan of the next batch: returns 1 and fills *plan, 0 once training is over,
+ * DASO_EINVAL if the previous epoch's loss has not been reported yet. */
+int daso_schedule_next(daso_schedule* s, daso_batch_plan* plan);
+/* Report the training loss of the epoch whose last batch was just planned
+ * (DASO_EINVAL otherwise, or for a NaN loss). */
+int daso_schedule_end_epoch(daso_schedule* s, double loss);
+void daso_schedule_destroy(daso_schedule* s);
+
 /* Static, NUL-terminated description of a status code. */
 const char* daso_status_string(int status);
 

@@ -27,7 +27,8 @@ DASO_PACK_PRE_MERGE = 1
 DASO_EXCHANGE_F32 = 2
 
 EXPORTED = ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
-            "daso_fused_sync_step", "daso_plan_buckets", "daso_status_string", "daso_abi_version")
+            "daso_fused_sync_step", "daso_plan_buckets", "daso_schedule_create", "daso_schedule_next",
+            "daso_schedule_end_epoch", "daso_schedule_destroy", "daso_status_string", "daso_abi_version")
 BUCKET_CAP_ELEMS = 25 * 1024 * 1024 // 4  # 25 MiB of fp32
 
 
@@ -258,3 +259,79 @@ def fused_sync_step(grads, params, momentum, stale, buckets, lr, mu, weight_deca
     and momentum; writes wire, grad_avg and stats when given."""
     FusedStep(grads, params, momentum, stale, buckets, lr, mu, weight_decay, wire, grad_avg, stats,
               flags)(stream)
+
+
+# ------------------------------------------------- phase/schedule controller
+class daso_schedule_config(ctypes.Structure):
+    _fields_ = [("total_epochs", ctypes.c_int32), ("warmup_epochs", ctypes.c_int32),
+                ("cooldown_epochs", ctypes.c_int32), ("batches_per_epoch", ctypes.c_int32),
+                ("B_init", ctypes.c_int32), ("W_init", ctypes.c_int32), ("group_count", ctypes.c_int32),
+                ("local_rank", ctypes.c_int32), ("patience", ctypes.c_int32),
+                ("plateau_rel_tol", ctypes.c_double)]
+
+
+class daso_batch_plan(ctypes.Structure):
+    _fields_ = [("step", ctypes.c_int64), ("epoch", ctypes.c_int32), ("batch", ctypes.c_int32),
+                ("phase", ctypes.c_int32), ("B", ctypes.c_int32), ("W", ctypes.c_int32),
+                ("actions", ctypes.c_uint32), ("S", ctypes.c_int32), ("sync_group", ctypes.c_int32),
+                ("merge_group", ctypes.c_int32)]
+
+
+PHASE_WARMUP, PHASE_CYCLING, PHASE_COOLDOWN = 0, 1, 2
+ACT_SEND, ACT_MERGE, ACT_BLOCKING, ACT_RECV_BCAST = 1, 2, 4, 8
+
+
+def _schedule_fns():
+    lib = load()
+    if not getattr(lib, "_daso_schedule_typed", False):
+        lib.daso_schedule_create.argtypes = [ctypes.POINTER(daso_schedule_config), ctypes.POINTER(ctypes.c_void_p)]
+        lib.daso_schedule_create.restype = ctypes.c_int
+        lib.daso_schedule_next.argtypes = [ctypes.c_void_p, ctypes.POINTER(daso_batch_plan)]
+        lib.daso_schedule_next.restype = ctypes.c_int
+        lib.daso_schedule_end_epoch.argtypes = [ctypes.c_void_p, ctypes.c_double]
+        lib.daso_schedule_end_epoch.restype = ctypes.c_int
+        lib.daso_schedule_destroy.argtypes = [ctypes.c_void_p]
+        lib.daso_schedule_destroy.restype = None
+        lib._daso_schedule_typed = True
+    return lib
+
+
+class Schedule:
+    """DASO's phase and exchange schedule for one GPU (daso_schedule_* in daso.h).
+
+    next_batch() returns the plan of the next batch as a dict (None once
+    training is over); end_epoch(loss) reports each epoch's training loss."""
+
+    def __init__(self, total_epochs: int, warmup_epochs: int, cooldown_epochs: int, batches_per_epoch: int,
+                 B_init: int, W_init: int = 0, group_count: int = 1, local_rank: int = 0, patience: int = 1,
+                 plateau_rel_tol: float = 0.0):
+        self._lib = _schedule_fns()
+        self.config = daso_schedule_config(total_epochs, warmup_epochs, cooldown_epochs, batches_per_epoch, B_init,
+                                           W_init, group_count, local_rank, patience, float(plateau_rel_tol))
+        h = ctypes.c_void_p()
+        _check(self._lib.daso_schedule_create(ctypes.byref(self.config), ctypes.byref(h)), "daso_schedule_create")
+        self._h = h
+        self._plan = daso_batch_plan()
+
+    def next_batch(self):
+        rc = self._lib.daso_schedule_next(self._h, ctypes.byref(self._plan))
+        if rc == 0:
+            return None
+        if rc < 0:
+            raise DasoError(rc, "daso_schedule_next")
+        p = self._plan
+        return {f: getattr(p, f) for f, _ in daso_batch_plan._fields_}
+
+    def end_epoch(self, loss: float) -> None:
+        _check(self._lib.daso_schedule_end_epoch(self._h, float(loss)), "daso_schedule_end_epoch")
+
+    def close(self) -> None:
+        if self._h:
+            self._lib.daso_schedule_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

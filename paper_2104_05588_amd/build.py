@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdaso.so")
 
-SOURCES = ["daso_kernels.hip", "daso_api.hip"]
+SOURCES = ["daso_kernels.hip", "daso_api.hip", "daso_schedule.cpp"]
 
 # Numerics flags: binary32 operations must be evaluated exactly as written (no
 # contraction into FMA, correctly rounded division, subnormals kept), so the

@@ -58,7 +58,9 @@ def test_struct_layouts_match_header(tmp_path):
     import subprocess
     fields = {"daso_bucket": [f[0] for f in L.daso_bucket._fields_],
               "daso_bucket_stats": [f[0] for f in L.daso_bucket_stats._fields_],
-              "daso_sync_args": [f[0] for f in L.daso_sync_args._fields_]}
+              "daso_sync_args": [f[0] for f in L.daso_sync_args._fields_],
+              "daso_schedule_config": [f[0] for f in L.daso_schedule_config._fields_],
+              "daso_batch_plan": [f[0] for f in L.daso_batch_plan._fields_]}
     src = ["#include <stdio.h>", "#include <stddef.h>", '#include "daso.h"', "int main(void) {"]
     for st, names in fields.items():
         src.append(f'  printf("{st} size %zu\\n", sizeof({st}));')
