@@ -187,6 +187,14 @@ def main() -> int:
         ts.sort()
         return ts[len(ts) // 2] * 1e-3
 
+    # the fused step with the fp32 exchange (copies and wire fp32), on fresh copies
+    st32 = [t.view(torch.bfloat16).float() for t in inp["stale"]]
+    wire32 = torch.empty(n, dtype=torch.float32, device="cuda")
+    step32 = daso.FusedStep(inp["grads"], inp["params"], inp["momentum"], st32, bks, w.lr, w.mu, w.wd,
+                            wire=wire32, stats=stats)
+    t_f32 = time_call(step32)
+    del step32, st32, wire32
+
     gavg = torch.empty(n, dtype=torch.float32, device="cuda")
     t_avg = time_call(lambda: daso.local_avg(inp["grads"], gavg))
     t_pack = time_call(lambda: daso.pack_bf16(inp["params"], wire))
@@ -196,6 +204,8 @@ def main() -> int:
         "daso_local_avg": {"us": t_avg * 1e6, "GBps": n * (4 * w.g + 4) / t_avg / 1e9},
         "daso_pack_bf16": {"us": t_pack * 1e6, "GBps": n * 6 / t_pack / 1e9},
         "daso_global_merge+wire": {"us": t_merge * 1e6, "GBps": n * (10 + 2 * w.P) / t_merge / 1e9},
+        "daso_fused_sync_step, fp32 exchange": {"us": t_f32 * 1e6,
+                                                "GBps": n * (4 * w.g + 4 * w.P + 20) / t_f32 / 1e9},
     }
 
     bpp = R.algorithmic_bytes_per_param(w.g, w.P)
