@@ -41,14 +41,18 @@
  *    only; the caller may free or reuse them as soon as the call returns.
  *  - Work is enqueued on `stream` (0 = the null stream) and runs asynchronously;
  *    no call synchronises the device or the stream.
- *  - n == 0 is a valid no-op: after the checks that do not involve n, the call
- *    returns DASO_OK and touches no buffer (statistics included).
+ *  - n == 0 is a valid no-op: once the counts and flags are checked the call
+ *    returns DASO_OK without looking at any pointer or buffer (statistics
+ *    included), so empty buffers may be NULL.
  *  - On any error nothing is launched and a negative status is returned; the
  *    buffers are untouched.  daso_status_string names the status.
  *  - Calls may be made from several host threads.  Fused steps with statistics
  *    share one small per-(device, stream) workspace that the library allocates on
- *    first use and keeps until the process ends; calls on one stream are ordered
- *    by that stream.
+ *    first use (and enlarges when a larger call needs it) and keeps until the
+ *    process ends; calls on one stream are ordered by that stream.  A call that
+ *    allocates cannot be captured into a HIP graph: make one call of the largest
+ *    size on the capturing stream before capturing; captured calls then launch
+ *    kernels only.
  */
 #ifndef DASO_H
 #define DASO_H

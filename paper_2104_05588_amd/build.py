@@ -14,6 +14,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdaso.so")
+CAPI_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "fused_step_capi.c")
+CAPI_CLIENT = os.path.join(PKG, "fused_step_capi")  # next to libdaso.so (found through $ORIGIN)
 
 SOURCES = ["daso_kernels.hip", "daso_api.hip", "daso_schedule.cpp"]
 
@@ -52,7 +54,23 @@ def build(verbose: bool = False) -> str:
     if verbose and errs:
         sys.stderr.write("\n".join(errs) + "\n")
     os.replace(tmp, LIB)
+    if os.path.exists(CAPI_CLIENT_SRC):
+        build_capi_client(verbose)
     return LIB
+
+
+def build_capi_client(verbose: bool = False) -> str:
+    """The plain C test client of the ABI (tests/c), linked against libdaso.so."""
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE, "-I", "/opt/rocm/include",
+           CAPI_CLIENT_SRC, "-o", CAPI_CLIENT, "-L", PKG, "-ldaso", "-L", "/opt/rocm/lib", "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN", "-Wl,-rpath,/opt/rocm/lib"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"gcc failed with status {res.returncode}")
+    return CAPI_CLIENT
 
 
 if __name__ == "__main__":

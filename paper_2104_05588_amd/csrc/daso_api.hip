@@ -237,13 +237,13 @@ const char* daso_status_string(int status) {
 
 int daso_local_avg(const float* const* grads, int32_t g, float* out, int64_t n, hipStream_t stream) {
   if (n < 0 || g < 1 || g > DASO_MAX_G) return DASO_EINVAL;
+  if (n == 0) return DASO_OK;
   int rc = check_ptr_table(reinterpret_cast<const void* const*>(grads), g);
   if (rc != DASO_OK) return rc;
   if ((rc = check_out(out)) != DASO_OK) return rc;
   const Span so = span_of(out, n, 4);
   for (int32_t r = 0; r < g; ++r)
     if (grads[r] != out && overlaps(so, span_of(grads[r], n, 4))) return DASO_EALIAS;
-  if (n == 0) return DASO_OK;
 
   StepArgs a;
   memset(&a, 0, sizeof(a));
@@ -256,11 +256,11 @@ int daso_local_avg(const float* const* grads, int32_t g, float* out, int64_t n, 
 
 int daso_pack_bf16(const float* src, uint16_t* wire, int64_t n, hipStream_t stream) {
   if (n < 0) return DASO_EINVAL;
+  if (n == 0) return DASO_OK;
   int rc = check_out(src);
   if (rc != DASO_OK) return rc;
   if ((rc = check_out(wire)) != DASO_OK) return rc;
   if (overlaps(span_of(src, n, 4), span_of(wire, n, 2))) return DASO_EALIAS;
-  if (n == 0) return DASO_OK;
 
   StepArgs a;
   memset(&a, 0, sizeof(a));
@@ -278,11 +278,11 @@ namespace {
 int merge_impl(float* params, const void* const* stale, int32_t P, const daso_bucket* buckets, int32_t nbuckets,
                void* wire, int64_t n, size_t esz, hipStream_t stream) {
   if (n < 0 || P < 0 || P > DASO_MAX_P) return DASO_EINVAL;
+  if (n == 0) return DASO_OK;
   int rc = check_out(params);
   if (rc != DASO_OK) return rc;
   if ((rc = check_ptr_table(stale, P)) != DASO_OK) return rc;
   if (wire && !aligned16(wire)) return DASO_EALIGN;
-  if (n == 0) return DASO_OK;
   if ((rc = check_buckets(buckets, nbuckets, n)) != DASO_OK) return rc;
   const Span sx = span_of(params, n, 4);
   for (int32_t i = 0; i < P; ++i)
@@ -331,6 +331,7 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
   const size_t esz = xf32 ? 4 : 2;
   if (xf32 ? (s.stale != nullptr || s.wire != nullptr) : (s.stale_f32 != nullptr || s.wire_f32 != nullptr))
     return DASO_EINVAL;
+  if (s.n == 0) return DASO_OK;
   int rc = check_ptr_table(reinterpret_cast<const void* const*>(s.grads), s.g);
   if (rc != DASO_OK) return rc;
   if ((rc = check_ptr_table(stale, s.P)) != DASO_OK) return rc;
@@ -339,7 +340,6 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
   if (wire && !aligned16(wire)) return DASO_EALIGN;
   if (s.grad_avg && !aligned16(s.grad_avg)) return DASO_EALIGN;
   if (s.stats && (reinterpret_cast<uintptr_t>(s.stats) & 7u) != 0) return DASO_EALIGN;
-  if (s.n == 0) return DASO_OK;
   if ((rc = check_buckets(s.buckets, s.nbuckets, s.n)) != DASO_OK) return rc;
 
   // outputs: params and momentum (in place), wire, grad_avg, stats

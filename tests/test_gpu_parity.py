@@ -454,3 +454,95 @@ def test_fused_f32_exchange(case):
                              exchange="f32")
     got = run_fused(inp, bks, wd=wd, flags=flags, gavg="new", f32=True)
     compare_fused(got, want, f"fused f32 {case}", gavg=True)
+
+
+# ----------------------------------------------------------- edge cases
+def test_empty_inputs_launch_nothing():
+    announce("n = 0 on every entry point")
+    e = torch.empty(0, dtype=torch.float32, device="cuda")
+    h = torch.empty(0, dtype=torch.int16, device="cuda")
+    daso.local_avg([e, e], e)
+    daso.pack_bf16(e, h)
+    daso.global_merge(e, [h, h], [(0, 0, 1)], h)
+    daso.fused_sync_step([e], e, e.clone(), [h], [(0, 0, 2)], 0.1, 0.9, 0.0, h, None, daso.new_stats(1))
+    torch.cuda.synchronize()
+
+
+def test_fused_beyond_int32_element_count():
+    """n = 2^31 + 13 elements (g = 1, P = 1, 37 GB of streams): element offsets
+    and tile counts past 32 bits; sampled elements around 2^31 and the ends
+    are checked against the oracle one by one."""
+    n = (1 << 31) + 13
+    announce("fused n =", n)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2104)
+    x = torch.randn(n, generator=gen, device="cuda") * 0.02
+    m = torch.zeros(n, device="cuda")
+    gr = torch.randn(n, generator=gen, device="cuda") * 1e-3
+    st = (x + torch.randn(n, generator=gen, device="cuda") * 1e-4).to(torch.bfloat16).view(torch.int16)
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    cut = (1 << 31) - 5   # bucket boundary just below 2^31, not vector aligned
+    bks = [(0, cut, 1), (cut, n - cut, 3)]
+    idx = np.unique(np.concatenate([np.arange(0, 16), np.arange(cut - 16, cut + 16), np.arange((1 << 31) - 16,
+                                    (1 << 31) + 13), np.random.default_rng(3).integers(0, n, 4096)]))
+    it = torch.from_numpy(idx).to("cuda")
+    take = lambda t: t.index_select(0, it).cpu().numpy()  # noqa: E731
+    s_x, s_m, s_g, s_s = take(x), take(m), take(gr), take(st).view(np.uint16)
+    st_dev = daso.new_stats(2)
+    daso.fused_sync_step([gr], x, m, [st], bks, 0.1, 0.9, 0.0, wire, None, st_dev)
+    torch.cuda.synchronize()
+    s_bks, i0 = [], 0
+    side = idx >= cut
+    for i in range(1, len(idx) + 1):
+        if i == len(idx) or side[i] != side[i0]:
+            s_bks.append((i0, i - i0, 3 if side[i0] else 1))
+            i0 = i
+    want = O.fused_sync_step([s_g], s_x, s_m, [s_s], s_bks, 0.1, 0.9)
+    check_f32(take(x), want["params"], "n > 2^31 params")
+    check_f32(take(m), want["momentum"], "n > 2^31 momentum")
+    check_u16(take(wire).view(np.uint16), want["wire"], "n > 2^31 wire")
+    got = daso.decode_stats(st_dev)
+    assert got[0][2] == 0 and got[1][2] == 0 and got[0][0] > 0 and got[1][1] > 0
+
+
+def test_fused_step_replays_in_a_hip_graph():
+    """After a first eager call (which allocates the statistics workspace), the
+    fused step can be captured in a graph: every replay, with eager work and
+    synchronisations between replays, gives the eager result bit for bit."""
+    rng = np.random.default_rng(77)
+    n = 300_001
+    bks = random_buckets(rng, n, 3)
+    inp = random_inputs(rng, n, 4, 8)
+    announce("fused step in a HIP graph")
+    grads = [dev_f32(a) for a in inp["grads"]]
+    stale = [dev_bf16(a) for a in inp["stale"]]
+    x0, m0 = dev_f32(inp["params"]), dev_f32(inp["momentum"])
+    x, m = x0.clone(), m0.clone()
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    stats = daso.new_stats(len(bks))
+    step = daso.FusedStep(grads, x, m, stale, bks, 0.1, 0.9, 0.0, wire=wire, stats=stats)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()                  # eager call on the capturing stream: allocates its workspace
+    torch.cuda.synchronize()
+    eager = (x.clone(), m.clone(), wire.clone(), stats.clone())
+    x.copy_(x0)
+    m.copy_(m0)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        x.copy_(x0)
+        m.copy_(m0)
+        wire.fill_(0)
+        stats.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(x.view(torch.int32), eager[0].view(torch.int32)), rep
+        assert torch.equal(m.view(torch.int32), eager[1].view(torch.int32)), rep
+        assert torch.equal(wire, eager[2]), rep
+        assert torch.equal(stats.view(torch.int64), eager[3].view(torch.int64)), rep
