@@ -47,12 +47,13 @@
  *  - On any error nothing is launched and a negative status is returned; the
  *    buffers are untouched.  daso_status_string names the status.
  *  - Calls may be made from several host threads.  Fused steps with statistics
- *    share one small per-(device, stream) workspace that the library allocates on
- *    first use (and enlarges when a larger call needs it) and keeps until the
- *    process ends; calls on one stream are ordered by that stream.  A call that
- *    allocates cannot be captured into a HIP graph: make one call of the largest
- *    size on the capturing stream before capturing; captured calls then launch
- *    kernels only.
+ *    share one small per-(device, stream) workspace (24 bytes per 2048
+ *    parameters) that the library allocates on first use, replaces by a larger
+ *    one when a larger call needs it, and never frees before the process ends;
+ *    calls on one stream are ordered by that stream.  A call that allocates
+ *    cannot be captured into a HIP graph: make one call of the largest size on
+ *    the capturing stream before capturing; captured calls then launch kernels
+ *    only, and stay valid when later calls enlarge the workspace.
  */
 #ifndef DASO_H
 #define DASO_H

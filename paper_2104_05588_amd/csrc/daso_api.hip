@@ -53,8 +53,11 @@ int check_buckets(const daso_bucket* b, int32_t nb, int64_t n) {
 
 // ---------------------------------------------------------------- workspace
 // Per (device, stream): the per-tile statistics partials of a fused launch.
-// Allocated on first use and grown when a larger launch needs it; every launch
-// writes each partial it later reads, so the contents never need clearing.
+// Allocated on first use and replaced by one at least twice as large when a
+// larger launch needs it.  A replaced buffer is never freed: launches already
+// queued, and graphs captured earlier, may still use it; the doubling keeps the
+// total within twice the largest buffer.  Every launch writes each partial it
+// later reads, so the contents never need clearing.
 struct Workspace {
   void* ptr = nullptr;
   size_t bytes = 0;
@@ -69,18 +72,10 @@ int workspace_for(hipStream_t stream, size_t need, void** out) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   Workspace& w = g_ws[{dev, stream}];
   if (w.bytes < need) {
-    if (w.ptr) {
-      // earlier launches on this stream may still read the old buffer
-      if (hipStreamSynchronize(stream) != hipSuccess) return DASO_EHIP;
-      (void)hipFree(w.ptr);
-      w.ptr = nullptr;
-      w.bytes = 0;
-    }
-    size_t bytes = std::max<size_t>(need, size_t(1) << 20);
-    if (hipMalloc(&w.ptr, bytes) != hipSuccess) {
-      w.ptr = nullptr;
-      return DASO_EHIP;
-    }
+    const size_t bytes = std::max<size_t>({need, 2 * w.bytes, size_t(1) << 20});
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return DASO_EHIP;
+    w.ptr = p;  // the previous buffer, if any, stays allocated (see above)
     w.bytes = bytes;
   }
   *out = w.ptr;
