@@ -535,6 +535,16 @@ def test_fused_step_replays_in_a_hip_graph():
         step()
     torch.cuda.synchronize()
     for rep in range(3):
+        if rep == 1:
+            # a larger eager call on the same stream enlarges the statistics
+            # workspace; the graph keeps using the buffer it captured
+            big = 5_000_000
+            bx, bm = torch.zeros(big, device="cuda"), torch.zeros(big, device="cuda")
+            bg = [torch.zeros(big, device="cuda")]
+            with torch.cuda.stream(side):
+                daso.fused_sync_step(bg, bx, bm, [], [(0, big, 1)], 0.1, 0.9, 0.0, None, None, daso.new_stats(1))
+            torch.cuda.synchronize()
+            del bx, bm, bg
         x.copy_(x0)
         m.copy_(m0)
         wire.fill_(0)
