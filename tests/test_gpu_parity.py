@@ -538,7 +538,7 @@ def test_fused_step_replays_in_a_hip_graph():
         if rep == 1:
             # a larger eager call on the same stream enlarges the statistics
             # workspace; the graph keeps using the buffer it captured
-            big = 5_000_000
+            big = 100_000_000   # 48,829 tiles: more partials than the first 1 MB workspace holds
             bx, bm = torch.zeros(big, device="cuda"), torch.zeros(big, device="cuda")
             bg = [torch.zeros(big, device="cuda")]
             with torch.cuda.stream(side):
