@@ -17,7 +17,7 @@ LIB = os.path.join(PKG, "libdaso.so")
 CAPI_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "fused_step_capi.c")
 CAPI_CLIENT = os.path.join(PKG, "fused_step_capi")  # next to libdaso.so (found through $ORIGIN)
 
-SOURCES = ["daso_kernels.hip", "daso_api.hip", "daso_schedule.cpp"]
+SOURCES = ["daso_kernels.hip", "daso_api.hip", "daso_host.cpp", "daso_schedule.cpp"]
 
 # Numerics flags: binary32 operations must be evaluated exactly as written (no
 # contraction into FMA, correctly rounded division, subnormals kept), so the
