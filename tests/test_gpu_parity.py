@@ -556,3 +556,32 @@ def test_fused_step_replays_in_a_hip_graph():
         assert torch.equal(m.view(torch.int32), eager[1].view(torch.int32)), rep
         assert torch.equal(wire, eager[2]), rep
         assert torch.equal(stats.view(torch.int64), eager[3].view(torch.int64)), rep
+
+
+def test_buckets_on_concurrent_streams():
+    """Bucket-granular use, as when buckets become ready one after another in
+    backpropagation: each bucket's fused step runs on its own stream, on views
+    of the flat buffers (every tensor starts at a multiple of 8 elements, so the
+    views stay 16-byte aligned).  Together they equal one whole-buffer step."""
+    w = R.workload("resnet18")
+    inp = Gen.host_inputs(w)
+    announce("fused step per bucket on", len(w.buckets), "streams")
+    grads = [dev_f32(a) for a in inp["grads"]]
+    stale = [dev_bf16(a) for a in inp["stale"]]
+    x, m = dev_f32(inp["params"]), dev_f32(inp["momentum"])
+    wire = torch.empty(w.n, dtype=torch.int16, device="cuda")
+    streams = [torch.cuda.Stream() for _ in w.buckets]
+    stats = [daso.new_stats(1) for _ in w.buckets]
+    torch.cuda.synchronize()
+    for bk, s, st in zip(w.buckets, streams, stats):
+        sl = slice(bk.start, bk.start + bk.numel)
+        with torch.cuda.stream(s):
+            daso.fused_sync_step([g[sl] for g in grads], x[sl], m[sl], [t[sl] for t in stale], [(0, bk.numel, bk.S)],
+                                 w.lr, w.mu, w.wd, wire[sl], None, st)
+    torch.cuda.synchronize()
+    bks = [(b.start, b.numel, b.S) for b in w.buckets]
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, w.lr, w.mu, w.wd)
+    check_f32(host_f32(x), want["params"], "per-bucket params")
+    check_f32(host_f32(m), want["momentum"], "per-bucket momentum")
+    check_u16(host_u16(wire), want["wire"], "per-bucket wire")
+    check_stats([daso.decode_stats(st)[0] for st in stats], want["stats"], "per-bucket stats")
