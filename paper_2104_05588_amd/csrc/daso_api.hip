@@ -58,18 +58,18 @@ struct Group {
 };
 
 // Cut the caller's bucket table into launches of at most kLaunchBuckets buckets.
-std::vector<Group> group_buckets(const daso_bucket* b, int32_t nb) {
+std::vector<Group> group_buckets(const daso_bucket* b, int32_t nb, int64_t tile) {
   std::vector<Group> out;
   for (int32_t i = 0; i < nb; i += daso::kLaunchBuckets) {
     Group gr{i, std::min<int32_t>(daso::kLaunchBuckets, nb - i), 0};
     for (int32_t k = 0; k < gr.count; ++k)
-      gr.ntiles += daso::tiles_of(b[i + k].start, b[i + k].start + b[i + k].numel);
+      gr.ntiles += daso::tiles_of(b[i + k].start, b[i + k].start + b[i + k].numel, tile);
     out.push_back(gr);
   }
   return out;
 }
 
-void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr) {
+void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr, int64_t tile) {
   int64_t t = 0;
   for (int32_t k = 0; k < gr.count; ++k) {
     const daso_bucket& s = b[gr.first + k];
@@ -77,7 +77,7 @@ void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr) {
     a.b[k].end = s.start + s.numel;
     a.b[k].first_tile = static_cast<int32_t>(t);
     a.b[k].S = s.S;
-    t += daso::tiles_of(s.start, s.start + s.numel);
+    t += daso::tiles_of(s.start, s.start + s.numel, tile);
   }
   a.nb = gr.count;
   // A launch needs at least one workgroup, even over empty buckets, so that
@@ -85,39 +85,16 @@ void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr) {
   a.ntiles = static_cast<int32_t>(std::max<int64_t>(t, 1));
 }
 
-// Compute units of the current device (cached per device).
-int compute_units() {
-  static std::mutex mu;
-  static std::map<int, int> cache;
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  std::lock_guard<std::mutex> lock(mu);
-  auto it = cache.find(dev);
-  if (it != cache.end()) return it->second;
-  int n = 0;
-  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) n = 0;
-  cache[dev] = n;
-  return n;
-}
-
-// Workgroups for a launch of `ntiles` tiles: one per tile, or a fixed number
-// per compute unit that take the tiles in turn.
-int grid_for(int32_t ntiles) {
-  if (daso::kBlocksPerCU <= 0) return ntiles;
-  const int cus = compute_units();
-  if (cus <= 0) return ntiles;
-  return static_cast<int>(std::min<int64_t>(ntiles, int64_t(cus) * daso::kBlocksPerCU));
-}
-
 int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
                daso_bucket_stats* stats, hipStream_t stream) {
-  const std::vector<Group> groups = group_buckets(b, nb);
+  const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
+  const int64_t tile = daso::tile_elems(mode, with_stats, a);
+  const std::vector<Group> groups = group_buckets(b, nb, tile);
   int64_t max_tiles = 1;
   for (const auto& gr : groups) {
     if (gr.ntiles > INT32_MAX) return DASO_EINVAL;
     max_tiles = std::max(max_tiles, gr.ntiles);
   }
-  const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
   int streams = 2;
   if (mode == daso::kModeAvg) streams = a.g + 1;
   if (mode == daso::kModeMerge) streams = a.P + 2 + (a.wire ? 1 : 0);
@@ -130,9 +107,9 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     a.partials = static_cast<TilePartial*>(ws);
   }
   for (const auto& gr : groups) {
-    fill_group(a, b, gr);
+    fill_group(a, b, gr, tile);
     a.stats = with_stats ? stats + gr.first : nullptr;
-    if (daso::launch_step(mode, with_stats, a, grid_for(a.ntiles), stream) != hipSuccess) return DASO_EHIP;
+    if (daso::launch_step(mode, with_stats, a, stream) != hipSuccess) return DASO_EHIP;
   }
   return DASO_OK;
 }

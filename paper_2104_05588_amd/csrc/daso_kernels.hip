@@ -347,13 +347,24 @@ constexpr bool batched() {
   return G > 0 && PP >= 0;
 }
 
-// Vectors per batch: as many as DASO_BATCH allows while the batch's input
-// registers stay within about 48 VGPRs per vector.
+// Vectors per thread and tile: a batch of kBatch when a vector's inputs fit in
+// 48 VGPRs, else one (measured: 2048-element tiles are best for the 40-register
+// resnet50 step, 1024-element tiles for the 56- and 104-register ones); the
+// runtime-count instances take kGenericIters vectors one after the other.
 template <int MODE, int G, int PP, bool XF>
-constexpr int batch_of() {
-  using V = VecIn<MODE, G, PP, XF>;
-  constexpr int regs = 4 * V::kG + (XF ? 4 : 2) * V::kP + ((MODE == kModeFused) ? 8 : 4);
-  return regs <= 48 ? kBatch : 1;
+constexpr int iters_of() {
+  if constexpr (!batched<MODE, G, PP>()) {
+    return kGenericIters;
+  } else {
+    using V = VecIn<MODE, G, PP, XF>;
+    constexpr int regs = 4 * V::kG + (XF ? 4 : 2) * V::kP + ((MODE == kModeFused) ? 8 : 4);
+    return regs <= 48 ? kBatch : 1;
+  }
+}
+
+template <int MODE, int G, int PP, bool XF>
+constexpr int64_t tile_of() {
+  return int64_t(kBlock) * kVec * iters_of<MODE, G, PP, XF>();
 }
 
 // ------------------------------------------------------------------- tiles
@@ -361,21 +372,17 @@ template <int MODE, int G, int PP, bool STATS, bool XF>
 __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64_t tlo, int64_t thi, float two_s,
                                          const Divisor& qg, const Divisor& qm, Acc& acc) {
   constexpr bool kBatched = batched<MODE, G, PP>();
+  constexpr int kIters = iters_of<MODE, G, PP, XF>();
   const int64_t t0 = abase + int64_t(threadIdx.x) * kVec;
   if constexpr (kBatched) {
-    if (tlo == abase && thi == abase + kTile) {
-      constexpr int B = batch_of<MODE, G, PP, XF>();
-      static_assert(kIters % B == 0, "batch must divide the iterations");
-      for (int it = 0; it < kIters; it += B) {
-        VecIn<MODE, G, PP, XF> v[B];
+    if (tlo == abase && thi == abase + tile_of<MODE, G, PP, XF>()) {
+      // a whole tile: all loads of the thread's kIters vectors, then the stores
+      VecIn<MODE, G, PP, XF> v[kIters];
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-          load_in<MODE, G, PP, XF, true>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b]);
+      for (int b = 0; b < kIters; ++b) load_in<MODE, G, PP, XF, true>(a, t0 + int64_t(b) * kBlock * kVec, 0xFu, v[b]);
 #pragma unroll
-        for (int b = 0; b < B; ++b)
-          finish<MODE, G, PP, XF, true, STATS>(a, t0 + int64_t(it + b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm,
-                                               acc);
-      }
+      for (int b = 0; b < kIters; ++b)
+        finish<MODE, G, PP, XF, true, STATS>(a, t0 + int64_t(b) * kBlock * kVec, 0xFu, v[b], two_s, qg, qm, acc);
       return;
     }
   }
@@ -415,10 +422,10 @@ __device__ __forceinline__ int xcd_ordered(int w, int grid) {
   return x * q + (x < r ? x : r) + (w >> 3);
 }
 
-// Workgroups take tiles w, w + gridDim.x, ...; the grid is either one workgroup
-// per tile or a few workgroups per compute unit.
+// One workgroup per tile; the loop also serves a grid smaller than the tiles.
 template <int MODE, int G, int PP, bool STATS, bool XF>
 __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
+  constexpr int64_t kTile = tile_of<MODE, G, PP, XF>();
   const int P = (PP >= 0) ? PP : a.P;
   const Divisor qg = make_divisor((G > 0) ? G : a.g);
   const int w0 = a.xcd_order ? xcd_ordered(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x))
@@ -476,63 +483,86 @@ __global__ __launch_bounds__(kBlock) void stats_kernel(const StepArgs a) {
   }
 }
 
-template <int MODE, int G, int PP, bool STATS, bool XF = false>
-hipError_t launch(const StepArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS, XF>), dim3(grid), dim3(kBlock), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !STATS) return e;
-  hipLaunchKernelGGL(stats_kernel, dim3(a.nb), dim3(kBlock), 0, stream, a);
-  return hipGetLastError();
-}
-
-template <bool STATS>
-hipError_t launch_fused(const StepArgs& a, int grid, hipStream_t stream) {
-  // Fully unrolled instances for common (g, P); any other pair takes the
-  // runtime-count instance, which computes the same bits.
+template <bool STATS, typename F>
+auto dispatch_fused(const StepArgs& a, const F& f) {
   if (a.xf32) {
-    if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS, true>(a, grid, stream);
-    return launch<kModeFused, 0, -1, STATS, true>(a, grid, stream);
+    if (a.g == 4 && a.P == 8) return f.template run<kModeFused, 4, 8, STATS, true>();
+    return f.template run<kModeFused, 0, -1, STATS, true>();
   }
-  if (a.g == 4 && a.P == 2) return launch<kModeFused, 4, 2, STATS>(a, grid, stream);
-  if (a.g == 4 && a.P == 4) return launch<kModeFused, 4, 4, STATS>(a, grid, stream);
-  if (a.g == 4 && a.P == 8) return launch<kModeFused, 4, 8, STATS>(a, grid, stream);
-  if (a.g == 4 && a.P == 16) return launch<kModeFused, 4, 16, STATS>(a, grid, stream);
-  if (a.g == 8 && a.P == 32) return launch<kModeFused, 8, 32, STATS>(a, grid, stream);
-  return launch<kModeFused, 0, -1, STATS>(a, grid, stream);
+  if (a.g == 4 && a.P == 2) return f.template run<kModeFused, 4, 2, STATS, false>();
+  if (a.g == 4 && a.P == 4) return f.template run<kModeFused, 4, 4, STATS, false>();
+  if (a.g == 4 && a.P == 8) return f.template run<kModeFused, 4, 8, STATS, false>();
+  if (a.g == 4 && a.P == 16) return f.template run<kModeFused, 4, 16, STATS, false>();
+  if (a.g == 8 && a.P == 32) return f.template run<kModeFused, 8, 32, STATS, false>();
+  return f.template run<kModeFused, 0, -1, STATS, false>();
 }
 
-}  // namespace
-
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, int grid, hipStream_t stream) {
+// The instance for a call, chosen in one place: `f.template run<MODE, G, PP,
+// STATS, XF>()` is called for it, both to launch and to size the tiles, so the
+// two always agree.  Fully unrolled instances exist for common stream counts;
+// any other count takes the runtime-count instance, which computes the same bits.
+template <typename F>
+auto dispatch(Mode mode, bool with_stats, const StepArgs& a, const F& f) {
   switch (mode) {
     case kModeAvg:
       switch (a.g) {
-        case 1: return launch<kModeAvg, 1, -1, false>(a, grid, stream);
-        case 2: return launch<kModeAvg, 2, -1, false>(a, grid, stream);
-        case 4: return launch<kModeAvg, 4, -1, false>(a, grid, stream);
-        case 8: return launch<kModeAvg, 8, -1, false>(a, grid, stream);
-        default: return launch<kModeAvg, 0, -1, false>(a, grid, stream);
+        case 1: return f.template run<kModeAvg, 1, -1, false, false>();
+        case 2: return f.template run<kModeAvg, 2, -1, false, false>();
+        case 4: return f.template run<kModeAvg, 4, -1, false, false>();
+        case 8: return f.template run<kModeAvg, 8, -1, false, false>();
+        default: return f.template run<kModeAvg, 0, -1, false, false>();
       }
     case kModePack:
-      return launch<kModePack, 0, -1, false>(a, grid, stream);
+      return f.template run<kModePack, 0, -1, false, false>();
     case kModeMerge:
       if (a.xf32) {
-        if (a.P == 8) return launch<kModeMerge, 0, 8, false, true>(a, grid, stream);
-        return launch<kModeMerge, 0, -1, false, true>(a, grid, stream);
+        if (a.P == 8) return f.template run<kModeMerge, 0, 8, false, true>();
+        return f.template run<kModeMerge, 0, -1, false, true>();
       }
       switch (a.P) {
-        case 0: return launch<kModeMerge, 0, 0, false>(a, grid, stream);
-        case 2: return launch<kModeMerge, 0, 2, false>(a, grid, stream);
-        case 4: return launch<kModeMerge, 0, 4, false>(a, grid, stream);
-        case 8: return launch<kModeMerge, 0, 8, false>(a, grid, stream);
-        case 16: return launch<kModeMerge, 0, 16, false>(a, grid, stream);
-        case 32: return launch<kModeMerge, 0, 32, false>(a, grid, stream);
-        default: return launch<kModeMerge, 0, -1, false>(a, grid, stream);
+        case 0: return f.template run<kModeMerge, 0, 0, false, false>();
+        case 2: return f.template run<kModeMerge, 0, 2, false, false>();
+        case 4: return f.template run<kModeMerge, 0, 4, false, false>();
+        case 8: return f.template run<kModeMerge, 0, 8, false, false>();
+        case 16: return f.template run<kModeMerge, 0, 16, false, false>();
+        case 32: return f.template run<kModeMerge, 0, 32, false, false>();
+        default: return f.template run<kModeMerge, 0, -1, false, false>();
       }
     case kModeFused:
-      return with_stats ? launch_fused<true>(a, grid, stream) : launch_fused<false>(a, grid, stream);
+    default:
+      if (with_stats) return dispatch_fused<true>(a, f);
+      return dispatch_fused<false>(a, f);
   }
-  return hipErrorInvalidValue;
+}
+
+struct Launcher {
+  const StepArgs& a;
+  hipStream_t stream;
+  template <int MODE, int G, int PP, bool STATS, bool XF>
+  hipError_t run() const {
+    hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS, XF>), dim3(a.ntiles), dim3(kBlock), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !STATS) return e;
+    hipLaunchKernelGGL(stats_kernel, dim3(a.nb), dim3(kBlock), 0, stream, a);
+    return hipGetLastError();
+  }
+};
+
+struct TileSize {
+  template <int MODE, int G, int PP, bool STATS, bool XF>
+  int64_t run() const {
+    return tile_of<MODE, G, PP, XF>();
+  }
+};
+
+}  // namespace
+
+int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& a) {
+  return dispatch(mode, with_stats, a, TileSize{});
+}
+
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, hipStream_t stream) {
+  return dispatch(mode, with_stats, a, Launcher{a, stream});
 }
 
 }  // namespace daso

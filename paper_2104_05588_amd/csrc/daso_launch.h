@@ -10,37 +10,30 @@
 namespace daso {
 
 // Work decomposition.  A launch covers up to kLaunchBuckets buckets.  Each bucket
-// [start, end) is cut into tiles of kTile elements aligned to kVec-element
-// vectors (the first tile of a bucket starts at the bucket start rounded down to
-// a vector boundary and is clipped to the bucket); a 256-thread workgroup
-// processes a tile as kIters vectors of kVec elements per thread.
+// [start, end) is cut into tiles aligned to kVec-element vectors (the first tile
+// of a bucket starts at the bucket start rounded down to a vector boundary and
+// is clipped to the bucket); one 256-thread workgroup processes one tile, each
+// thread one batch of vectors whose loads are all issued before any store.  The
+// batch, and so the tile, depends on the kernel instance: two vectors per thread
+// (2048-element tiles) when a vector's inputs take at most 48 registers, one
+// (1024-element tiles) otherwise.  tile_elems() tells the host which.
+//
 // Tuning parameters (compile-time; the defaults are the measured best on MI355X).
-#ifndef DASO_TILE_ITERS
-#define DASO_TILE_ITERS 2
-#endif
 #ifndef DASO_BATCH
 #define DASO_BATCH 2
-#endif
-#ifndef DASO_BLOCKS_PER_CU
-#define DASO_BLOCKS_PER_CU 0
 #endif
 #ifndef DASO_NT_PARAMS
 #define DASO_NT_PARAMS 1
 #endif
-#ifndef DASO_BLOCK
-#define DASO_BLOCK 256
-#endif
-constexpr int kBlock = DASO_BLOCK;
+constexpr int kBlock = 256;
 constexpr int kVec = 4;
-constexpr int kIters = DASO_TILE_ITERS;
-constexpr int kBatch = DASO_BATCH;           // vectors whose loads are issued together
-constexpr int kBlocksPerCU = DASO_BLOCKS_PER_CU;  // 0: one workgroup per tile
-constexpr bool kNtParams = DASO_NT_PARAMS != 0;   // non-temporal access to params/momentum
+constexpr int kBatch = DASO_BATCH;               // most vectors per thread and tile
+constexpr bool kNtParams = DASO_NT_PARAMS != 0;  // non-temporal access to params/momentum
+constexpr int kGenericIters = 2;                 // vectors per thread for runtime stream counts
+constexpr int kLaunchBuckets = 64;
 // Streams (inputs + outputs) from which each XCD is given a contiguous run of
 // tiles; measured: a gain with 42 streams, a loss with 17 and 25.
 constexpr int kXcdOrderMinStreams = 32;
-constexpr int64_t kTile = int64_t(kBlock) * kVec * kIters;
-constexpr int kLaunchBuckets = 64;
 
 enum Mode : int { kModeAvg = 0, kModePack = 1, kModeMerge = 2, kModeFused = 3 };
 
@@ -82,15 +75,19 @@ struct StepArgs {
   TileBucket b[kLaunchBuckets];
 };
 
-// Number of tiles bucket [start, end) is cut into.
-inline int64_t tiles_of(int64_t start, int64_t end) {
+// Number of tiles of `tile` elements bucket [start, end) is cut into.
+inline int64_t tiles_of(int64_t start, int64_t end, int64_t tile) {
   if (end <= start) return 0;
   const int64_t a = start & ~int64_t(kVec - 1);
-  return (end - a + kTile - 1) / kTile;
+  return (end - a + tile - 1) / tile;
 }
 
-// Enqueue one launch of `mode` over the buckets in `args` with `grid`
-// workgroups (1 <= grid <= args.ntiles), which take the tiles in turn.
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, int grid, hipStream_t stream);
+// Elements per tile of the kernel instance that launch_step picks for these
+// arguments (mode, stream counts, exchange type).
+int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& args);
+
+// Enqueue one launch of `mode` over the buckets in `args`, one workgroup per
+// tile (args.ntiles, counted with tile_elems()).
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, hipStream_t stream);
 
 }  // namespace daso
