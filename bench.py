@@ -214,7 +214,7 @@ def main() -> int:
     traffic = counter_traffic(w.name)
 
     out = {
-        "metric": "params synced/sec per fused DASO sync step (with achieved HBM GB/s as % of peak)",
+        "metric": "params synced/sec and achieved HBM GB/s (% of peak) per fused DASO sync step",
         "value": n * args.steps / wall,
         "unit": "params/s",
         "n_gpus": 1,
@@ -224,12 +224,12 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 (bf16 wire and stale copies)",
+        "dtype": "f32",
         "data": "synthetic: seeded device-generated params/grads/stale copies shaped like the network",
         "config": {"workload": f"{w.name}-shaped fused DASO sync step", "params": n,
                    "tensors": len(w.numels), "buckets": len(bks), "g": w.g, "P": w.P,
                    "S": sorted({b.S for b in w.buckets}), "lr": w.lr, "mu": w.mu, "wd": w.wd,
-                   "wire": "bf16", "stats": True, "parallelism": "single GPU"},
+                   "wire": "bf16", "stale_copies": "bf16", "stats": True, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": traffic,
                      "kernel": "step_kernel<fused> + stats_kernel tail (one call per step; HIP events bracket both)",
