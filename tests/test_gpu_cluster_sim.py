@@ -1,0 +1,79 @@
+"""DASO end to end on one GPU: a cluster of simulated nodes, each driven by the
+native schedule through DasoSync, with exchanges simulated as buffer hand-offs
+that land S batches later.  Every node's parameters and momentum must equal,
+bit for bit, the same simulation built from the CPU oracle and the reference
+schedule."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2104_05588_amd as daso
+from oracle import daso_oracle as O
+from oracle import daso_schedule as OS
+
+pytestmark = pytest.mark.gpu
+F32 = np.float32
+
+
+def test_simulated_cluster_matches_oracle():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nodes, g, n = 4, 4, 40_003
+    spans = [(0, 15_001), (15_001, n - 15_001)]
+    E, warm, cool, nb = 6, 1, 1, 6
+    cfg = dict(total_epochs=E, warmup_epochs=warm, cooldown_epochs=cool, batches_per_epoch=nb, B_init=4,
+               W_init=2, group_count=1, local_rank=0, patience=1, plateau_rel_tol=0.0)
+    losses = [1.0, 0.9, 0.9, 0.9, 0.8, 0.8]          # plateaus in the cycling epochs change B and W
+    plans_ref = OS.plan_training(OS.Config(**cfg), losses)
+
+    rng = np.random.default_rng(2021)
+    x0 = [(rng.standard_normal(n) * 0.02).astype(F32) for _ in range(nodes)]
+    grads_all = [[[(rng.standard_normal(n) * 1e-3).astype(F32) for _ in range(g)] for _ in range(nodes)]
+                 for _ in range(E * nb)]
+
+    # GPU side
+    syncs = [daso.DasoSync(daso.Schedule(**cfg), torch.from_numpy(x0[k].copy()).cuda(),
+                           torch.zeros(n, device="cuda"), spans, 0.1, 0.9) for k in range(nodes)]
+    sent = {}
+    # oracle side
+    xs = [x.copy() for x in x0]
+    ms = [np.zeros(n, F32) for _ in range(nodes)]
+    sent_ref = {}
+
+    kinds = set()
+    for t in range(E * nb):
+        plans = [s.next_plan() for s in syncs]
+        ref = plans_ref[t]
+        assert all(p == ref for p in plans), (t, plans[0], ref)
+        acts = ref["actions"]
+        kinds.add(acts)
+        merge = bool(acts & OS.MERGE)
+        S = ref["S"] if merge else 0
+        bks = [(s, k, S) for (s, k) in spans]
+        grads_dev = [[torch.from_numpy(a).cuda() for a in grads_all[t][k]] for k in range(nodes)]
+        for k in range(nodes):
+            syncs[k].step(ref, grads_dev[k], arrived=sent[t - S] if merge else None)
+            out = O.fused_sync_step(grads_all[t][k], xs[k], ms[k], sent_ref[t - S] if merge else [], bks, 0.1, 0.9)
+            xs[k], ms[k] = out["params"], out["momentum"]
+            if acts & (OS.SEND | OS.BLOCKING):
+                syncs[k].wire_ref = out["wire"]
+        if acts & OS.BLOCKING:
+            copies = [s.wire.clone() for s in syncs]
+            copies_ref = [s.wire_ref for s in syncs]
+            for k in range(nodes):
+                syncs[k].blocking_average(copies)
+                xs[k] = O.global_merge(xs[k], copies_ref, [(s, kk, 0) for (s, kk) in spans])[0]
+        if acts & OS.SEND:
+            sent[t] = [s.wire.clone() for s in syncs]
+            sent_ref[t] = [s.wire_ref for s in syncs]
+        if ref["batch"] == nb - 1:
+            for s in syncs:
+                s.end_epoch(losses[ref["epoch"]])
+    torch.cuda.synchronize()
+    assert {OS.BLOCKING, OS.SEND, OS.MERGE, 0} <= kinds | {0}, kinds
+    for k in range(nodes):
+        assert np.array_equal(syncs[k].params.cpu().numpy().view(np.uint32), xs[k].view(np.uint32)), k
+        assert np.array_equal(syncs[k].momentum.cpu().numpy().view(np.uint32), ms[k].view(np.uint32)), k
+    # the cluster stays together: after the blocking cool-down every node holds the same state
+    for k in range(1, nodes):
+        assert np.array_equal(xs[k], xs[0])
