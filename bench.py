@@ -195,6 +195,15 @@ def main() -> int:
     t_f32 = time_call(step32)
     del step32, st32, wire32
 
+    # the batches of the cycling phase without copies to merge: the local step
+    # alone, and the local step packing the wire for an exchange
+    local = daso.FusedStep(inp["grads"], inp["params"], inp["momentum"], [], [(0, n, 0)], w.lr, w.mu, w.wd)
+    t_local = time_call(local)
+    send = daso.FusedStep(inp["grads"], inp["params"], inp["momentum"], [], [(0, n, 0)], w.lr, w.mu, w.wd,
+                          wire=wire)
+    t_send = time_call(send)
+    del local, send
+
     gavg = torch.empty(n, dtype=torch.float32, device="cuda")
     t_avg = time_call(lambda: daso.local_avg(inp["grads"], gavg))
     t_pack = time_call(lambda: daso.pack_bf16(inp["params"], wire))
@@ -206,6 +215,10 @@ def main() -> int:
         "daso_global_merge+wire": {"us": t_merge * 1e6, "GBps": n * (10 + 2 * w.P) / t_merge / 1e9},
         "daso_fused_sync_step, fp32 exchange": {"us": t_f32 * 1e6,
                                                 "GBps": n * (4 * w.g + 4 * w.P + 20) / t_f32 / 1e9},
+        "daso_fused_sync_step, local step only (P=0)": {"us": t_local * 1e6,
+                                                        "GBps": n * (4 * w.g + 16) / t_local / 1e9},
+        "daso_fused_sync_step, local step + bf16 wire (P=0)": {"us": t_send * 1e6,
+                                                               "GBps": n * (4 * w.g + 18) / t_send / 1e9},
     }
 
     bpp = R.algorithmic_bytes_per_param(w.g, w.P)

@@ -489,6 +489,15 @@ auto dispatch_fused(const StepArgs& a, const F& f) {
     if (a.g == 4 && a.P == 8) return f.template run<kModeFused, 4, 8, STATS, true>();
     return f.template run<kModeFused, 0, -1, STATS, true>();
   }
+  if (a.P == 0) {  // the local step of most cycling batches (no copies arrive)
+    switch (a.g) {
+      case 1: return f.template run<kModeFused, 1, 0, STATS, false>();
+      case 2: return f.template run<kModeFused, 2, 0, STATS, false>();
+      case 4: return f.template run<kModeFused, 4, 0, STATS, false>();
+      case 8: return f.template run<kModeFused, 8, 0, STATS, false>();
+      default: break;
+    }
+  }
   if (a.g == 4 && a.P == 2) return f.template run<kModeFused, 4, 2, STATS, false>();
   if (a.g == 4 && a.P == 4) return f.template run<kModeFused, 4, 4, STATS, false>();
   if (a.g == 4 && a.P == 8) return f.template run<kModeFused, 4, 8, STATS, false>();

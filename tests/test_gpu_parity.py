@@ -585,3 +585,19 @@ def test_buckets_on_concurrent_streams():
     check_f32(host_f32(m), want["momentum"], "per-bucket momentum")
     check_u16(host_u16(wire), want["wire"], "per-bucket wire")
     check_stats([daso.decode_stats(st)[0] for st in stats], want["stats"], "per-bucket stats")
+
+
+@pytest.mark.parametrize("g", [1, 2, 4, 8])
+def test_fused_local_step_only(g):
+    """P = 0: the local step of a cycling batch without arrivals, with and
+    without packing the wire (the batch that starts an exchange)."""
+    rng = np.random.default_rng(600 + g)
+    n = 70_001
+    bks = random_buckets(rng, n, 3)
+    inp = random_inputs(rng, n, g, 0)
+    announce("fused local step g=", g)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], [], bks, 0.1, 0.9)
+    got = run_fused(inp, bks)
+    compare_fused(got, want, f"local step g={g}")
+    got = run_fused(inp, bks, wire=False, stats=False)
+    compare_fused(got, want, f"local step g={g} bare", wire=False, stats=False)
