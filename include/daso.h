@@ -185,12 +185,12 @@ int32_t daso_plan_buckets(const int64_t* numels, int32_t ntensors, int64_t cap_e
  * blocking global synchronisation after every batch; the cycling phase in
  * between uses non-blocking synchronisation: a global exchange starts every B
  * batches and its copies are merged W batches later with S = W in Eq. (1).  B is
- * set by hand; W starts at B/4.  Each time the training loss plateaus, B and W
- * halve (down to 1); once both are 1 and the loss plateaus again they return to
- * their initial values.  The role of global synchronisation rotates between the
- * groups (the GPUs with the same local rank on every node): exchange k is done
- * by group k mod group_count, whose member then broadcasts the merged state to
- * the other GPUs of its node.
+ * set by hand; W starts at a quarter of B.  Whenever the loss stops improving, B
+ * and W are halved, never below 1; a further plateau with both at 1 restores
+ * their starting values.  The groups (the GPUs with the same local rank on every
+ * node) take turns at the exchange: exchange k is done by group k mod
+ * group_count, whose member then hands the merged state to the other GPUs of its
+ * node.
  *
  * Readings where the paper is silent: a plateau is `patience` consecutive
  * cycling epochs whose loss does not fall below best - plateau_rel_tol * |best|

@@ -30,8 +30,8 @@ order so that a GPU implementation can reproduce the same bits:
      16-bit type while the send buffer is packed and cast back on receipt;
      Section 4: DASO uses bfloat16): wire = bf16_rne(x').
 
-The fp32 exchange (Section 3: in the non-blocking case casting does not pay,
-since it delays the start of the communication) keeps the same arithmetic with
+The fp32 exchange (Section 3: without blocking, the cast would only hold back
+the send, so the parameters go out uncast) keeps the same arithmetic with
 binary32 copies: widen() is the identity and the wire is x' itself.
 
 Readings taken where the paper is silent (each also listed in the design

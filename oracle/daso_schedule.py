@@ -11,11 +11,11 @@ What the paper states:
   * in cycling, B forward-backward passes separate global synchronisations and
     the exchanged states are used W batches later, merged by Eq. (1) with S = W;
   * B is set by hand, W starts at B/4;
-  * each time the training loss plateaus, B and W halve, down to one; when both
-    are one and the loss plateaus, both return to their initial values;
-  * the role of global synchronisation rotates between the groups (one GPU per
-    node with the same local rank), and the member that synchronised broadcasts
-    the result to the other GPUs of its node.
+  * whenever the loss stops improving B and W are halved, never below one; a
+    further plateau with both at one restores their starting values;
+  * the groups (one GPU per node with the same local rank) take turns at the
+    global exchange, and the member that merged hands the result to the other
+    GPUs of its node.
 
 Readings where the text is silent (the same as the library's):
   * W starts at max(1, B // 4) unless given;
