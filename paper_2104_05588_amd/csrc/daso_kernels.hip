@@ -237,19 +237,22 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
 #pragma unroll
     for (int r = 1; r < g; ++r) s = s + load_f32<FULL, true>(a.grads[r], e0, mask);
     gbar = divide(s, qg);
+    if constexpr (MODE == kModeAvg) {
+      store_f32<FULL, true>(a.gavg, e0, mask, gbar);
+      return;
+    }
     if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
-    if constexpr (MODE == kModeAvg) return;
   }
 
-  f32x4 x = load_f32<FULL, false>(a.x, e0, mask);
+  f32x4 x = load_f32<FULL, kNtParams>(a.x, e0, mask);
   f32x4 xl = x;
   if constexpr (MODE == kModeFused) {
-    const f32x4 m = load_f32<FULL, false>(a.m, e0, mask);
+    const f32x4 m = load_f32<FULL, kNtParams>(a.m, e0, mask);
     f32x4 d = gbar;
     if (a.wd != 0.0f) d = gbar + (a.wd * x);
     const f32x4 m_new = (a.mu * m) + d;
     xl = x - (a.lr * m_new);
-    store_f32<FULL, false>(a.m, e0, mask, m_new);
+    store_f32<FULL, kNtParams>(a.m, e0, mask, m_new);
   }
 
   f32x4 xn = xl;
@@ -259,7 +262,7 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
     for (int i = 0; i < P; ++i) acc4 = acc4 + received<XF>(load_x<XF, FULL>(a.stale[i], e0, mask));
     xn = divide(acc4, qm);
   }
-  store_f32<FULL, false>(a.x, e0, mask, xn);
+  store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
   if (a.wire) {
     const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
     store_wire<XF, FULL>(a.wire, e0, mask, pre ? xl : xn);
@@ -430,7 +433,8 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   const Divisor qg = make_divisor((G > 0) ? G : a.g);
   const int w0 = a.xcd_order ? xcd_ordered(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x))
                              : static_cast<int>(blockIdx.x);
-  for (int tile = w0; tile < a.ntiles; tile += static_cast<int>(gridDim.x)) {
+  for (int64_t t = w0; t < a.ntiles; t += gridDim.x) {
+    const int tile = static_cast<int>(t);
     // bucket owning this tile: the last one whose first tile is <= tile
     int lo = 0, hi = a.nb - 1;
     while (lo < hi) {
