@@ -168,3 +168,21 @@ def test_native_controller_rejects_misuse():
         s.end_epoch(float("nan"))
     s.end_epoch(1.0)
     assert s.next_batch()["epoch"] == 1
+
+
+def test_driver_checks_copies_against_the_plan():
+    """DasoSync refuses copies on a batch that does not merge, and requires them
+    on one that does, before any kernel is launched (host-side check)."""
+    import torch
+    import paper_2104_05588_amd as daso
+    from paper_2104_05588_amd import _lib as L
+    x = torch.zeros(64)
+    sync = daso.DasoSync(daso.Schedule(1, 0, 0, 4, 1), x, torch.zeros(64), [(0, 64)], 0.1, 0.9)
+    grads = [torch.zeros(64)]
+    copy = torch.zeros(64, dtype=torch.int16)
+    no_merge = {"actions": L.ACT_SEND, "S": -1}
+    merge = {"actions": L.ACT_MERGE, "S": 1}
+    with pytest.raises(ValueError):
+        sync.step(no_merge, grads, arrived=[copy])
+    with pytest.raises(ValueError):
+        sync.step(merge, grads)
