@@ -271,6 +271,32 @@ def test_fused_random(case):
     compare_fused(got, want, f"fused {case}", gavg=gavg != "none")
 
 
+HYPER_CASES = [
+    # (seed, n, g, P, lr, mu, wd, S choices): other optimizer constants, large S
+    (31, 40_000, 4, 8, 0.05, 0.5, 5e-4, (0, 4, 12, 100)),
+    (32, 40_000, 4, 8, 1e-3, 0.0, 0.0, (1, 3, 1000)),
+    (33, 20_001, 8, 32, 1.7, 0.99, 1e-5, (1, 2, 4, 8, 16)),
+    (34, 20_001, 3, 7, 0.0, 0.9, 0.0, (0, 5, 999)),
+    (35, 9_999, 1, 0, 0.3, 0.95, 1e-2, (0,)),
+    (36, 65_536, 2, 4, 0.1, 0.9, 0.0, (2, 6, 30, 62)),
+]
+
+
+@pytest.mark.parametrize("case", HYPER_CASES, ids=[f"s{c[0]}_lr{c[4]}_mu{c[5]}" for c in HYPER_CASES])
+def test_fused_other_constants_and_large_S(case):
+    """lr, mu and wd other than the workloads' (mu = 0, lr = 0 included) and
+    staleness up to 1000, with 2S + P both powers of two and not."""
+    seed, n, g, P, lr, mu, wd, S_choices = case
+    rng = np.random.default_rng(seed)
+    bks = random_buckets(rng, n, 5, S_choices)
+    inp = random_inputs(rng, n, g, P)
+    announce("fused constants", case)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                             lr, mu, wd)
+    got = run_fused(inp, bks, lr=lr, mu=mu, wd=wd, gavg="new")
+    compare_fused(got, want, f"fused constants {case}", gavg=True)
+
+
 @pytest.mark.parametrize("seed", [21, 22, 23])
 def test_fused_special_values(seed):
     """NaN, infinities, subnormals, the largest finite values and signed zeros
