@@ -40,15 +40,17 @@
  *  - Host pointer arrays (grads, stale) and bucket tables are read during the call
  *    only; the caller may free or reuse them as soon as the call returns.
  *  - Work is enqueued on `stream` (0 = the null stream) and runs asynchronously;
- *    no call synchronises the device or the stream.
+ *    no call synchronises the device or the stream.  The stream and every buffer
+ *    must belong to the calling thread's current device (hipSetDevice); a stream
+ *    of another device is rejected with DASO_EINVAL.
  *  - n == 0 is a valid no-op: once the counts and flags are checked the call
  *    returns DASO_OK without looking at any pointer or buffer (statistics
  *    included), so empty buffers may be NULL.
  *  - On any error nothing is launched and a negative status is returned; the
  *    buffers are untouched.  daso_status_string names the status.
  *  - Calls may be made from several host threads.  Fused steps with statistics
- *    share one small per-(device, stream) workspace (24 bytes per 2048
- *    parameters) that the library allocates on first use, replaces by a larger
+ *    share one small per-(device, stream) workspace (24 bytes per tile of 1024
+ *    or 2048 parameters) that the library allocates on first use, replaces by a larger
  *    one when a larger call needs it, and never frees before the process ends;
  *    calls on one stream are ordered by that stream.  A call that allocates
  *    cannot be captured into a HIP graph: make one call of the largest size on
@@ -68,7 +70,8 @@ extern "C" {
 
 /* status codes */
 #define DASO_OK 0
-#define DASO_EINVAL (-1)  /* null required pointer, bad count, S < 0, buckets not a tiling of [0,n) */
+#define DASO_EINVAL (-1)  /* null required pointer, bad count, S < 0, buckets not a tiling of [0,n),
+                             a stream of another device */
 #define DASO_EALIGN (-2)  /* a device base pointer is not 16-byte aligned */
 #define DASO_EALIAS (-3)  /* an output overlaps an input other than in the allowed in-place pairs */
 #define DASO_EHIP (-4)    /* a HIP call (launch, allocation of the stats workspace) failed */

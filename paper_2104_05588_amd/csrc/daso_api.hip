@@ -34,9 +34,7 @@ struct Workspace {
 std::mutex g_ws_mu;
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
-int workspace_for(hipStream_t stream, size_t need, void** out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return DASO_EHIP;
+int workspace_for(int dev, hipStream_t stream, size_t need, void** out) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
   Workspace& w = g_ws[{dev, stream}];
   if (w.bytes < need) {
@@ -85,8 +83,21 @@ void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr, int64_t tile
   a.ntiles = static_cast<int32_t>(std::max<int64_t>(t, 1));
 }
 
+// The current device, which must also be the device of `stream` (kernels run
+// on the stream's device and the buffers and workspace live on the current one).
+int current_device(hipStream_t stream, int* dev) {
+  if (hipGetDevice(dev) != hipSuccess) return DASO_EHIP;
+  if (stream == nullptr) return DASO_OK;
+  hipDevice_t sdev = 0;
+  if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return DASO_EHIP;
+  return sdev == *dev ? DASO_OK : DASO_EINVAL;
+}
+
 int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
                daso_bucket_stats* stats, hipStream_t stream) {
+  int dev = 0;
+  const int drc = current_device(stream, &dev);
+  if (drc != DASO_OK) return drc;
   const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
   const int64_t tile = daso::tile_elems(mode, with_stats, a);
   const std::vector<Group> groups = group_buckets(b, nb, tile);
@@ -102,7 +113,7 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   a.xcd_order = streams >= daso::kXcdOrderMinStreams ? 1 : 0;
   if (with_stats) {
     void* ws = nullptr;
-    const int rc = workspace_for(stream, static_cast<size_t>(max_tiles) * sizeof(TilePartial), &ws);
+    const int rc = workspace_for(dev, stream, static_cast<size_t>(max_tiles) * sizeof(TilePartial), &ws);
     if (rc != DASO_OK) return rc;
     a.partials = static_cast<TilePartial*>(ws);
   }
