@@ -70,7 +70,7 @@ extern "C" {
 
 /* status codes */
 #define DASO_OK 0
-#define DASO_EINVAL (-1)  /* null required pointer, bad count, S < 0, buckets not a tiling of [0,n),
+#define DASO_EINVAL (-1)  /* null required pointer, bad count, S outside [0, DASO_MAX_S], buckets not a tiling of [0,n),
                              a stream of another device */
 #define DASO_EALIGN (-2)  /* a device base pointer is not 16-byte aligned */
 #define DASO_EALIAS (-3)  /* an output overlaps an input other than in the allowed in-place pairs */
@@ -78,6 +78,7 @@ extern "C" {
 
 #define DASO_MAX_G 64     /* most replica gradients per call */
 #define DASO_MAX_P 64     /* most exchanged copies per call */
+#define DASO_MAX_S (1 << 20) /* largest staleness: 2S and 2S + P stay exact in binary32 */
 
 /* flags of daso_sync_args */
 #define DASO_PACK_PRE_MERGE 1u /* pack xl (after the optimizer step, before Eq. (1)) instead of x' */
@@ -85,7 +86,8 @@ extern "C" {
                                   wire_f32, both binary32 (no cast; the non-blocking case of
                                   Section 3); stale and wire must then be NULL */
 
-/* A bucket: elements [start, start + numel) merged with staleness S (S >= 0).
+/* A bucket: elements [start, start + numel) merged with staleness S
+ * (0 <= S <= DASO_MAX_S).
  * S is the number of batches the exchanged copies are late (Eq. (1)); S = 0
  * gives the plain average of the copies, as in blocking synchronisation. */
 typedef struct daso_bucket {

@@ -191,7 +191,7 @@ const char* daso_status_string(int status) {
   switch (status) {
     case DASO_OK: return "DASO_OK: success";
     case DASO_EINVAL:
-      return "DASO_EINVAL: invalid argument (null pointer, count out of range, S < 0, or buckets not tiling [0, n))";
+      return "DASO_EINVAL: invalid argument (null pointer, count out of range, S outside [0, DASO_MAX_S], buckets not tiling [0, n), or a stream of another device)";
     case DASO_EALIGN: return "DASO_EALIGN: a device buffer is not 16-byte aligned";
     case DASO_EALIAS: return "DASO_EALIAS: an output buffer overlaps another buffer";
     case DASO_EHIP: return "DASO_EHIP: a HIP call failed";

@@ -10,7 +10,7 @@
 namespace daso {
 namespace host {
 
-constexpr int32_t kMaxS = 1 << 20;  // 2S and 2S + P stay exact in binary32
+constexpr int32_t kMaxS = DASO_MAX_S;  // 2S and 2S + P stay exact in binary32
 
 // Buckets must tile [0, n): sorted by start they lie back to back; S in [0, kMaxS].
 int check_buckets(const daso_bucket* b, int32_t nb, int64_t n);

@@ -133,6 +133,9 @@ def test_global_merge_rejects(lib):
     assert f(A, st, 2, L.bucket_table([(0, 600, 1), (600, 401, 2)]), 2, None, n, None) == L.DASO_EINVAL
     assert f(A, st, 2, L.bucket_table([(0, 600, -1), (600, 400, 2)]), 2, None, n, None) == L.DASO_EINVAL
     assert f(A, st, 2, L.bucket_table([(0, 1000, 1 << 21)]), 1, None, n, None) == L.DASO_EINVAL
+    assert f(A, st, 2, L.bucket_table([(0, 1000, (1 << 20) + 1)]), 1, None, n, None) == L.DASO_EINVAL
+    # S = DASO_MAX_S passes the checks; with no GPU here the call then fails in HIP
+    assert f(A, st, 2, L.bucket_table([(0, 1000, 1 << 20)]), 1, None, n, None) == L.DASO_EHIP
     assert f(A, st, 2, ok_b, 0, None, n, None) == L.DASO_EINVAL
     bad = L.bucket_table([(0, 1000, 1)])
     bad[0].reserved = 3

@@ -279,6 +279,7 @@ HYPER_CASES = [
     (34, 20_001, 3, 7, 0.0, 0.9, 0.0, (0, 5, 999)),
     (35, 9_999, 1, 0, 0.3, 0.95, 1e-2, (0,)),
     (36, 65_536, 2, 4, 0.1, 0.9, 0.0, (2, 6, 30, 62)),
+    (37, 30_000, 4, 8, 0.1, 0.9, 0.0, (1 << 20, (1 << 20) - 3, 0)),   # the largest S accepted
 ]
 
 
