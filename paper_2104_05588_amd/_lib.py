@@ -109,6 +109,8 @@ def _ptr(t: Optional[torch.Tensor], dtypes: Tuple[torch.dtype, ...], n: int, wha
         return None
     if not t.is_cuda:
         raise ValueError(f"{what} must be a device tensor")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{what} is on {t.device}, not on the current device cuda:{torch.cuda.current_device()}")
     if t.dtype not in dtypes:
         raise ValueError(f"{what} must have dtype in {dtypes}, got {t.dtype}")
     if t.numel() != n or not t.is_contiguous():
@@ -227,6 +229,9 @@ class FusedStep:
             if not stats.is_cuda or stats.dtype != torch.float64 or tuple(stats.shape) != (len(buckets), 3) \
                     or not stats.is_contiguous():
                 raise ValueError("stats must be a contiguous float64 device tensor of shape [nbuckets, 3]")
+            if stats.device.index != torch.cuda.current_device():
+                raise ValueError(f"stats is on {stats.device}, not on the current device")
+        self._device = torch.cuda.current_device()
         a = daso_sync_args()
         a.n, a.g, a.P = n, len(grads), len(stale)
         a.grads = self._grads
@@ -250,6 +255,9 @@ class FusedStep:
         self._fn = load().daso_fused_sync_step
 
     def __call__(self, stream=None) -> None:
+        if torch.cuda.current_device() != self._device:
+            raise ValueError(f"prepared on cuda:{self._device}, called with cuda:{torch.cuda.current_device()} "
+                             "current")
         _check(self._fn(self._byref, _stream_handle(stream)), "daso_fused_sync_step")
 
 
