@@ -52,7 +52,8 @@
  *    share one small per-(device, stream) workspace (24 bytes per tile of 1024
  *    or 2048 parameters) that the library allocates on first use, replaces by a larger
  *    one when a larger call needs it, and never frees before the process ends;
- *    calls on one stream are ordered by that stream.  A call that allocates
+ *    calls on one stream are ordered by that stream, and threads may share a
+ *    stream (each call queues its kernels together).  A call that allocates
  *    cannot be captured into a HIP graph: make one call of the largest size on
  *    the capturing stream before capturing; captured calls then launch kernels
  *    only, and stay valid when later calls enlarge the workspace.

@@ -25,18 +25,26 @@ using daso::TilePartial;
 // larger launch needs it.  A replaced buffer is never freed: launches already
 // queued, and graphs captured earlier, may still use it; the doubling keeps the
 // total within twice the largest buffer.  Every launch writes each partial it
-// later reads, so the contents never need clearing.
+// later reads, so the contents never need clearing.  A call holds the entry's
+// lock from choosing the buffer until its last launch is queued, so that two
+// host threads sharing a stream cannot queue one call's step between the other
+// call's step and its statistics pass.
 struct Workspace {
+  std::mutex mu;
   void* ptr = nullptr;
   size_t bytes = 0;
 };
 
-std::mutex g_ws_mu;
+std::mutex g_ws_mu;  // guards the map itself; nodes never move or go away
 std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
-int workspace_for(int dev, hipStream_t stream, size_t need, void** out) {
+Workspace& workspace_entry(int dev, hipStream_t stream) {
   std::lock_guard<std::mutex> lock(g_ws_mu);
-  Workspace& w = g_ws[{dev, stream}];
+  return g_ws[{dev, stream}];
+}
+
+// With w.mu held: make w hold at least `need` bytes.
+int reserve(Workspace& w, size_t need) {
   if (w.bytes < need) {
     const size_t bytes = std::max<size_t>({need, 2 * w.bytes, size_t(1) << 20});
     void* p = nullptr;
@@ -44,7 +52,6 @@ int workspace_for(int dev, hipStream_t stream, size_t need, void** out) {
     w.ptr = p;  // the previous buffer, if any, stays allocated (see above)
     w.bytes = bytes;
   }
-  *out = w.ptr;
   return DASO_OK;
 }
 
@@ -111,11 +118,13 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   if (mode == daso::kModeMerge) streams = a.P + 2 + (a.wire ? 1 : 0);
   if (mode == daso::kModeFused) streams = a.g + a.P + 4 + (a.wire ? 1 : 0) + (a.gavg ? 1 : 0);
   a.xcd_order = streams >= daso::kXcdOrderMinStreams ? 1 : 0;
+  std::unique_lock<std::mutex> hold;
   if (with_stats) {
-    void* ws = nullptr;
-    const int rc = workspace_for(dev, stream, static_cast<size_t>(max_tiles) * sizeof(TilePartial), &ws);
+    Workspace& w = workspace_entry(dev, stream);
+    hold = std::unique_lock<std::mutex>(w.mu);
+    const int rc = reserve(w, static_cast<size_t>(max_tiles) * sizeof(TilePartial));
     if (rc != DASO_OK) return rc;
-    a.partials = static_cast<TilePartial*>(ws);
+    a.partials = static_cast<TilePartial*>(w.ptr);
   }
   for (const auto& gr : groups) {
     fill_group(a, b, gr, tile);

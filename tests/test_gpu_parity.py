@@ -614,6 +614,53 @@ def test_buckets_on_concurrent_streams():
     check_stats([daso.decode_stats(st)[0] for st in stats], want["stats"], "per-bucket stats")
 
 
+def test_calls_from_several_host_threads():
+    """Four host threads make fused calls with statistics at once, two of them
+    on one shared stream: every call must still see its own tile partials (a
+    call's step and statistics pass are queued together)."""
+    import threading
+    rng = np.random.default_rng(707)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    owner = [0, 0, 1, 2]                     # thread -> stream
+    jobs = []
+    for t in range(4):
+        for _ in range(12):
+            n = int(rng.integers(1_000, 200_000))
+            bks = random_buckets(rng, n, int(rng.integers(1, 4)))
+            inp = random_inputs(rng, n, 4, 8)
+            dev = {"grads": [dev_f32(a) for a in inp["grads"]], "stale": [dev_bf16(a) for a in inp["stale"]],
+                   "x": dev_f32(inp["params"]), "m": dev_f32(inp["momentum"]),
+                   "wire": torch.empty(n, dtype=torch.int16, device="cuda"), "stats": daso.new_stats(len(bks))}
+            jobs.append((t, bks, inp, dev))
+    torch.cuda.synchronize()
+    announce("fused calls from 4 host threads,", len(jobs), "calls, 2 threads sharing a stream")
+    start = threading.Barrier(4)
+    errors = []
+
+    def work(t):
+        try:
+            start.wait()
+            for (tt, bks, _, d) in jobs:
+                if tt == t:
+                    daso.fused_sync_step(d["grads"], d["x"], d["m"], d["stale"], bks, 0.1, 0.9, 0.0, d["wire"],
+                                         None, d["stats"], 0, streams[owner[t]])
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    th = [threading.Thread(target=work, args=(t,)) for t in range(4)]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for k, (t, bks, inp, d) in enumerate(jobs):
+        want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+        got = {"params": host_f32(d["x"]), "momentum": host_f32(d["m"]), "wire": host_u16(d["wire"]),
+               "grad_avg": None, "stats": daso.decode_stats(d["stats"])}
+        compare_fused(got, want, f"thread {t} call {k}")
+
+
 @pytest.mark.parametrize("g", [1, 2, 4, 8])
 def test_fused_local_step_only(g):
     """P = 0: the local step of a cycling batch without arrivals, with and
