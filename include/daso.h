@@ -56,7 +56,9 @@
  *    stream (each call queues its kernels together).  A call that allocates
  *    cannot be captured into a HIP graph: make one call of the largest size on
  *    the capturing stream before capturing; captured calls then launch kernels
- *    only, and stay valid when later calls enlarge the workspace.
+ *    only, and stay valid when later calls enlarge the workspace.  A captured
+ *    call keeps the capturing stream's workspace: its replays must not overlap
+ *    other calls on that stream, or each other.
  */
 #ifndef DASO_H
 #define DASO_H
