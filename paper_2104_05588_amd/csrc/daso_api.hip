@@ -15,6 +15,9 @@
 
 namespace {
 
+// Kernel arguments are passed by value and limited to 4 KB.
+static_assert(sizeof(daso::StepArgs) <= 4096, "StepArgs must fit the 4 KB kernel-argument limit");
+
 using daso::StepArgs;
 using daso::TileBucket;
 using daso::TilePartial;
