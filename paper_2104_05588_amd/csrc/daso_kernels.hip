@@ -418,11 +418,15 @@ __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64
 
 // ------------------------------------------------------------------- kernel
 // Workgroups are dispatched to the 8 XCDs of the chip in turn (workgroup w to
-// XCD w % 8).  xcd_ordered renumbers workgroup w so that each XCD walks a
-// contiguous run of the grid: a bijection of [0, grid).
-__device__ __forceinline__ int xcd_ordered(int w, int grid) {
-  const int q = grid >> 3, r = grid & 7, x = w & 7;
-  return x * q + (x < r ? x : r) + (w >> 3);
+// XCD w % 8).  xcd_runs renumbers workgroup w so that each XCD takes runs of
+// `run` consecutive tiles: the k-th workgroup of XCD x in block b (of 8 * run
+// tiles) gets tile b * 8 * run + x * run + k.  Workgroups past the last whole
+// block keep their number.  A bijection of [0, grid); run = 1 is the identity.
+__device__ __forceinline__ int xcd_runs(int w, int grid, int run) {
+  const int block = 8 * run;
+  if (w >= (grid / block) * block) return w;
+  const int j = w >> 3, x = w & 7;
+  return (j / run) * block + x * run + (j % run);
 }
 
 // One workgroup per tile; the loop also serves a grid smaller than the tiles.
@@ -431,8 +435,8 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   constexpr int64_t kTile = tile_of<MODE, G, PP, XF>();
   const int P = (PP >= 0) ? PP : a.P;
   const Divisor qg = make_divisor((G > 0) ? G : a.g);
-  const int w0 = a.xcd_order ? xcd_ordered(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x))
-                             : static_cast<int>(blockIdx.x);
+  const int w0 = a.xcd_run > 1 ? xcd_runs(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), a.xcd_run)
+                               : static_cast<int>(blockIdx.x);
   for (int64_t t = w0; t < a.ntiles; t += gridDim.x) {
     const int tile = static_cast<int>(t);
     // bucket owning this tile: the last one whose first tile is <= tile

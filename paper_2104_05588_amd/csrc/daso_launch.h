@@ -31,9 +31,14 @@ constexpr int kBatch = DASO_BATCH;               // most vectors per thread and 
 constexpr bool kNtParams = DASO_NT_PARAMS != 0;  // non-temporal access to params/momentum
 constexpr int kGenericIters = 2;                 // vectors per thread for runtime stream counts
 constexpr int kLaunchBuckets = 64;
-// Streams (inputs + outputs) from which each XCD is given a contiguous run of
-// tiles; measured: a gain with 42 streams, a loss with 17 and 25.
-constexpr int kXcdOrderMinStreams = 32;
+// Tile order across the 8 XCDs: workgroups go to the XCDs in turn, and a
+// launch touching many streams runs faster when each XCD takes runs of
+// consecutive tiles (measured: runs of 16 tiles +5.5% with 25 streams, runs of
+// 32 +1% with 45; with 17 or fewer streams plain order is as fast or faster).
+constexpr int kXcdRunMidStreams = 20;   // from here: runs of kXcdRunMid tiles
+constexpr int kXcdRunMid = 16;
+constexpr int kXcdRunManyStreams = 32;  // from here: runs of kXcdRunMany tiles
+constexpr int kXcdRunMany = 32;
 
 enum Mode : int { kModeAvg = 0, kModePack = 1, kModeMerge = 2, kModeFused = 3 };
 
@@ -70,7 +75,7 @@ struct StepArgs {
   uint32_t flags;
   int32_t nb;            // buckets in this launch
   int32_t ntiles;        // tiles in this launch
-  int32_t xcd_order;     // nonzero: renumber workgroups XCD-contiguously
+  int32_t xcd_run;       // > 1: each XCD takes runs of this many consecutive tiles
   int32_t xf32;          // nonzero: fp32 exchange (stale copies and wire are fp32)
   TileBucket b[kLaunchBuckets];
 };

@@ -255,6 +255,9 @@ FUSED_CASES = [
     (10, 50_001, 64, 64, 3, 0.0, 0, "new"),
     (11, 77_777, 4, 16, 5, 0.0, 0, "none"),
     (12, 12_345, 6, 3, 70, 0.0, 0, "none"),
+    # whole blocks of XCD tile runs: 45 streams (runs of 32 tiles), 26 streams (runs of 16)
+    (13, 2 * 256 * 1024 + 4_097, 8, 32, 4, 0.0, 0, "none"),
+    (14, 5 * 128 * 1024 + 333, 4, 16, 3, 0.0, 0, "new"),
 ]
 
 
