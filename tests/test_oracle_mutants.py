@@ -83,6 +83,25 @@ def _sgd_ignores_wd(x, m, gbar, lr, mu, wd):
     return x - (F32(lr) * m_new), m_new
 
 
+def _stats_count_nan_only(gbar, xl, x_new):
+    g, d, _ = _true_bucket_stats(gbar, xl, x_new)
+    return g, d, int(np.count_nonzero(np.isnan(x_new)))
+
+
+def _stats_sums_in_float32(gbar, xl, x_new):
+    g32 = np.asarray(gbar, dtype=np.float32)
+    d32 = np.asarray(x_new, dtype=np.float32) - np.asarray(xl, dtype=np.float32)
+    _, _, nf = _true_bucket_stats(gbar, xl, x_new)
+    return float(np.sum(g32 * g32)), float(np.sum(d32 * d32)), nf
+
+
+def _stats_abs_not_square(gbar, xl, x_new):
+    _, d, nf = _true_bucket_stats(gbar, xl, x_new)
+    return float(np.sum(np.abs(np.asarray(gbar, dtype=np.float64)))), d, nf
+
+
+_true_bucket_stats = O.bucket_stats
+
 MUTANTS = [
     ("merge_eq1", _merge_S_not_2S, [pins.test_merge_gradient_form_appendix,
                                     pins.test_merge_small_integers_match_exact_rational_eq1]),
@@ -98,6 +117,9 @@ MUTANTS = [
     ("sgd_momentum", _sgd_wrong_sign, [pins.test_sgd_matches_torch_optim_sgd]),
     ("sgd_momentum", _sgd_momentum_misplaced, [pins.test_sgd_matches_torch_optim_sgd]),
     ("sgd_momentum", _sgd_ignores_wd, [pins.test_sgd_matches_torch_optim_sgd]),
+    ("bucket_stats", _stats_count_nan_only, [pins.test_stats_count_nonfinite]),
+    ("bucket_stats", _stats_sums_in_float32, [pins.test_stats_match_exactly_rounded_sums]),
+    ("bucket_stats", _stats_abs_not_square, [pins.test_stats_match_exactly_rounded_sums]),
 ]
 
 
