@@ -167,6 +167,23 @@ def test_pack_every_high_half_and_specials():
     check_u16(host_u16(wire), O.pack_bf16(f), "pack")
 
 
+def test_pack_every_binary32_pattern():
+    """daso_pack_bf16 on all 2^32 binary32 bit patterns, in 32 launches of
+    2^27, against the oracle (which the host C check ties to the nearest-value
+    definition on every pattern)."""
+    chunk = 1 << 27
+    wire = torch.empty(chunk, dtype=torch.int16, device="cuda")
+    for c in range(32):
+        announce("pack_bf16 patterns", hex(c * chunk), "to", hex((c + 1) * chunk - 1))
+        bits = torch.arange(c * chunk, (c + 1) * chunk, dtype=torch.int64, device="cuda")
+        bits = torch.where(bits >= (1 << 31), bits - (1 << 32), bits).to(torch.int32)
+        daso.pack_bf16(bits.view(torch.float32), wire)
+        torch.cuda.synchronize()
+        del bits
+        u = np.arange(c * chunk, (c + 1) * chunk, dtype=np.uint64).astype(np.uint32)
+        check_u16(host_u16(wire), O.pack_bf16(u.view(F32)), f"pack patterns chunk {c}")
+
+
 @pytest.mark.parametrize("n", SIZES)
 def test_pack_sizes(n):
     announce("pack_bf16 n=", n)
