@@ -447,7 +447,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
       else hi = mid - 1;
     }
     const TileBucket bk = a.b[lo];
-    const int64_t abase = (bk.start & ~int64_t(kVec - 1)) + int64_t(tile - bk.first_tile) * kTile;
+    const int64_t abase = (bk.start / kTile + int64_t(tile - bk.first_tile)) * kTile;  // on the tile grid
     const int64_t tlo = bk.start > abase ? bk.start : abase;
     const int64_t thi = bk.end < abase + kTile ? bk.end : abase + kTile;
     const float two_s = static_cast<float>(2 * bk.S);

@@ -9,10 +9,10 @@
 
 namespace daso {
 
-// Work decomposition.  A launch covers up to kLaunchBuckets buckets.  Each bucket
-// [start, end) is cut into tiles aligned to kVec-element vectors (the first tile
-// of a bucket starts at the bucket start rounded down to a vector boundary and
-// is clipped to the bucket); one 256-thread workgroup processes one tile, each
+// Work decomposition.  A launch covers up to kLaunchBuckets buckets.  Tiles lie
+// on one grid counted from element 0 (see tiles_of); each bucket [start, end)
+// takes the grid tiles it overlaps, the first and last clipped to the bucket.
+// One 256-thread workgroup processes one tile, each
 // thread one batch of vectors whose loads are all issued before any store.  The
 // batch, and so the tile, depends on the kernel instance: two vectors per thread
 // (2048-element tiles) when a vector's inputs take at most 48 registers, one
@@ -80,11 +80,12 @@ struct StepArgs {
   TileBucket b[kLaunchBuckets];
 };
 
-// Number of tiles of `tile` elements bucket [start, end) is cut into.
+// Tiles lie on one grid of `tile` elements counted from element 0, so that a
+// wavefront's accesses start on whole cache lines wherever a bucket begins; a
+// bucket [start, end) takes the grid tiles it overlaps, clipped to its range.
 inline int64_t tiles_of(int64_t start, int64_t end, int64_t tile) {
   if (end <= start) return 0;
-  const int64_t a = start & ~int64_t(kVec - 1);
-  return (end - a + tile - 1) / tile;
+  return (end - 1) / tile - start / tile + 1;
 }
 
 // Elements per tile of the kernel instance that launch_step picks for these
