@@ -564,16 +564,19 @@ auto dispatch(Mode mode, bool with_stats, const StepArgs& a, const F& f) {
   }
 }
 
+// Launches report their own status (hipLaunchKernel's return value), so an
+// error left behind by an earlier, unrelated HIP call is neither blamed on
+// this call nor consumed by it.
 struct Launcher {
   const StepArgs& a;
   hipStream_t stream;
   template <int MODE, int G, int PP, bool STATS, bool XF>
   hipError_t run() const {
-    hipLaunchKernelGGL((step_kernel<MODE, G, PP, STATS, XF>), dim3(a.ntiles), dim3(kBlock), 0, stream, a);
-    hipError_t e = hipGetLastError();
+    void* args[] = {const_cast<StepArgs*>(&a)};
+    const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&step_kernel<MODE, G, PP, STATS, XF>),
+                                         dim3(a.ntiles), dim3(kBlock), args, 0, stream);
     if (e != hipSuccess || !STATS) return e;
-    hipLaunchKernelGGL(stats_kernel, dim3(a.nb), dim3(kBlock), 0, stream, a);
-    return hipGetLastError();
+    return hipLaunchKernel(reinterpret_cast<const void*>(&stats_kernel), dim3(a.nb), dim3(kBlock), args, 0, stream);
   }
 };
 

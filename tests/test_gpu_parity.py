@@ -634,6 +634,36 @@ def test_buckets_on_concurrent_streams():
     check_stats([daso.decode_stats(st)[0] for st in stats], want["stats"], "per-bucket stats")
 
 
+def test_earlier_hip_error_is_neither_blamed_nor_consumed():
+    """A failed HIP call made before (here an impossible hipMalloc) may leave its
+    error as the thread's last error: the next library call must still succeed
+    (its launches report their own status)."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so.7")          # the HIP runtime this process already uses
+    hip.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    rng = np.random.default_rng(808)
+    n = 10_001
+    bks = random_buckets(rng, n, 2)
+    inp = random_inputs(rng, n, 4, 8)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+    grads = [dev_f32(a) for a in inp["grads"]]
+    stale = [dev_bf16(a) for a in inp["stale"]]
+    x, m = dev_f32(inp["params"]), dev_f32(inp["momentum"])
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    st = daso.new_stats(len(bks))
+    torch.cuda.synchronize()
+    announce("fused step after a failed hipMalloc")
+    ptr = ctypes.c_void_p()
+    failed = hip.hipMalloc(ctypes.byref(ptr), ctypes.c_size_t(1 << 62))
+    assert failed != 0
+    daso.fused_sync_step(grads, x, m, stale, bks, 0.1, 0.9, 0.0, wire, None, st)
+    hip.hipGetLastError()                               # clear it before torch launches again
+    torch.cuda.synchronize()
+    got = {"params": host_f32(x), "momentum": host_f32(m), "wire": host_u16(wire), "grad_avg": None,
+           "stats": daso.decode_stats(st)}
+    compare_fused(got, want, "after a failed hipMalloc")
+
+
 def test_calls_from_several_host_threads():
     """Four host threads make fused calls with statistics at once, two of them
     on one shared stream: every call must still see its own tile partials (a
