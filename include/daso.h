@@ -159,8 +159,8 @@ int daso_global_merge(float* params, const uint16_t* const* stale, int32_t P,
                       const daso_bucket* buckets, int32_t nbuckets, uint16_t* wire,
                       int64_t n, hipStream_t stream);
 
-/* Eq. (1) for the fp32 exchange (Section 3: in the non-blocking case the
- * parameters travel uncast): as daso_global_merge, with P fp32 copies, and wire
+/* Eq. (1) for the fp32 exchange (Section 3: a non-blocking exchange sends the
+ * parameters uncast): as daso_global_merge, with P fp32 copies, and wire
  * (NULL, or n fp32) receiving the merged parameters. */
 int daso_global_merge_f32(float* params, const float* const* stale, int32_t P,
                           const daso_bucket* buckets, int32_t nbuckets, float* wire,

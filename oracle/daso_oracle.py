@@ -26,8 +26,8 @@ order so that a GPU implementation can reproduce the same bits:
      computed as a = (2S) * xl ; a = a + x_i for i = 1..P ; x' = a / (2S + P);
      with P = 0 the merge is the identity.  The x_i arrive as bf16 and are
      widened exactly (bits << 16).
-  4. buffer packaging for the exchange (Section 3: parameters are cast to a
-     16-bit type while the send buffer is packed and cast back on receipt;
+  4. buffer packaging for the exchange (Section 3: the send buffer holds a
+     16-bit rendering of the parameters, widened again by the receiver;
      Section 4: DASO uses bfloat16): wire = bf16_rne(x').
 
 The fp32 exchange (Section 3: without blocking, the cast would only hold back

@@ -5,7 +5,7 @@ controller; nothing in the product path imports it.
 
 What the paper states:
   * training has three phases over a fixed number of epochs: warm-up and
-    cool-down (a set number of epochs at the start and at the end) use blocking
+    cool-down (a chosen count of opening and closing epochs) use blocking
     global synchronisation; the cycling phase between them is non-blocking;
   * in the blocking case all synchronisation steps happen after each batch;
   * in cycling, B forward-backward passes separate global synchronisations and
