@@ -228,7 +228,7 @@ typedef struct daso_schedule_config {
   int32_t group_count;       /* >= 1: GPUs per node */
   int32_t local_rank;        /* 0..group_count-1: this GPU's group */
   int32_t patience;          /* >= 1 */
-  double plateau_rel_tol;    /* >= 0 */
+  double plateau_rel_tol;    /* finite, >= 0 */
 } daso_schedule_config;
 
 /* What this GPU does around one batch. */
@@ -247,7 +247,9 @@ typedef struct daso_batch_plan {
 
 typedef struct daso_schedule daso_schedule; /* opaque, owned by the caller through create/destroy */
 
-/* Create a controller; DASO_EINVAL for an invalid configuration. */
+/* Create a controller; DASO_EINVAL for an invalid configuration.  A controller
+ * keeps one GPU's state: calls on it from several threads need the caller's own
+ * locking.  daso_schedule_destroy(NULL) does nothing. */
 int daso_schedule_create(const daso_schedule_config* cfg, daso_schedule** out);
 /* Plan of the next batch: returns 1 and fills *plan, 0 once training is over,
  * DASO_EINVAL if the previous epoch's loss has not been reported yet. */

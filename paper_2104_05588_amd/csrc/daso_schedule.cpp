@@ -49,7 +49,8 @@ int daso_schedule_create(const daso_schedule_config* c, daso_schedule** out) {
   if (c->total_epochs < 1 || c->warmup_epochs < 0 || c->cooldown_epochs < 0 ||
       int64_t(c->warmup_epochs) + c->cooldown_epochs > c->total_epochs || c->batches_per_epoch < 1 ||
       c->B_init < 1 || c->W_init < 0 || c->W_init > c->B_init || c->group_count < 1 || c->local_rank < 0 ||
-      c->local_rank >= c->group_count || c->patience < 1 || !(c->plateau_rel_tol >= 0.0))
+      c->local_rank >= c->group_count || c->patience < 1 || !(c->plateau_rel_tol >= 0.0) ||
+      !std::isfinite(c->plateau_rel_tol))
     return DASO_EINVAL;
   daso_schedule* s = new (std::nothrow) daso_schedule();
   if (s == nullptr) return DASO_EINVAL;

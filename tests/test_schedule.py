@@ -151,6 +151,7 @@ def test_native_controller_rejects_misuse():
     from paper_2104_05588_amd import _lib as L
     for bad in [dict(total_epochs=0), dict(warmup_epochs=3, cooldown_epochs=3), dict(B_init=0),
                 dict(W_init=9), dict(local_rank=2), dict(patience=0), dict(plateau_rel_tol=-1.0),
+                dict(plateau_rel_tol=float("inf")), dict(plateau_rel_tol=float("nan")),
                 dict(batches_per_epoch=0)]:
         kw = dict(total_epochs=5, warmup_epochs=1, cooldown_epochs=1, batches_per_epoch=3, B_init=4,
                   group_count=2, local_rank=0)
