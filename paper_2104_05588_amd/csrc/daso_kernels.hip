@@ -219,7 +219,40 @@ __device__ __forceinline__ AccT<CountT> block_sum(AccT<CountT> v) {
   return r;
 }
 
+// ------------------------------------------- arithmetic shared by both paths
+// The local average's output: the local-average entry point stores it
+// (streaming); the fused step stores it only when asked for.
+template <int MODE, bool FULL>
+__device__ __forceinline__ void store_avg(const StepArgs& a, int64_t e0, unsigned mask, f32x4 gbar) {
+  if constexpr (MODE == kModeAvg) store_f32<FULL, true>(a.gavg, e0, mask, gbar);
+  else if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
+}
+
+// The optimizer step (Section 3.1; PyTorch SGD with momentum, coupled weight
+// decay that is skipped when zero): the local state xl; m becomes the new
+// momentum.
+__device__ __forceinline__ f32x4 sgd_momentum4(const StepArgs& a, f32x4 x, f32x4& m, f32x4 gbar) {
+  f32x4 d = gbar;
+  if (a.wd != 0.0f) d = gbar + (a.wd * x);
+  m = (a.mu * m) + d;
+  return x - (a.lr * m);
+}
+
+// The outputs after the merge: params, the wire (of x' or, with
+// DASO_PACK_PRE_MERGE, of xl) and the statistics.
+template <int MODE, bool FULL, bool STATS, bool XF>
+__device__ __forceinline__ void store_results(const StepArgs& a, int64_t e0, unsigned mask, f32x4 gbar, f32x4 xl,
+                                              f32x4 xn, Acc& acc) {
+  store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
+  if (a.wire) {
+    const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
+    store_wire<XF, FULL>(a.wire, e0, mask, pre ? xl : xn);
+  }
+  if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
+}
+
 // ----------------------------------------------------------- one 4-vector
+// Stream counts known only at run time: each input is folded in as it loads.
 template <int MODE, int G, int PP, bool FULL, bool STATS, bool XF>
 __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned mask, float two_s,
                                          const Divisor& qg, const Divisor& qm, Acc& acc) {
@@ -237,22 +270,16 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
 #pragma unroll
     for (int r = 1; r < g; ++r) s = s + load_f32<FULL, true>(a.grads[r], e0, mask);
     gbar = divide(s, qg);
-    if constexpr (MODE == kModeAvg) {
-      store_f32<FULL, true>(a.gavg, e0, mask, gbar);
-      return;
-    }
-    if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
+    store_avg<MODE, FULL>(a, e0, mask, gbar);
+    if constexpr (MODE == kModeAvg) return;
   }
 
-  f32x4 x = load_f32<FULL, kNtParams>(a.x, e0, mask);
+  const f32x4 x = load_f32<FULL, kNtParams>(a.x, e0, mask);
   f32x4 xl = x;
   if constexpr (MODE == kModeFused) {
-    const f32x4 m = load_f32<FULL, kNtParams>(a.m, e0, mask);
-    f32x4 d = gbar;
-    if (a.wd != 0.0f) d = gbar + (a.wd * x);
-    const f32x4 m_new = (a.mu * m) + d;
-    xl = x - (a.lr * m_new);
-    store_f32<FULL, kNtParams>(a.m, e0, mask, m_new);
+    f32x4 m = load_f32<FULL, kNtParams>(a.m, e0, mask);
+    xl = sgd_momentum4(a, x, m, gbar);
+    store_f32<FULL, kNtParams>(a.m, e0, mask, m);
   }
 
   f32x4 xn = xl;
@@ -262,12 +289,7 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
     for (int i = 0; i < P; ++i) acc4 = acc4 + received<XF>(load_x<XF, FULL>(a.stale[i], e0, mask));
     xn = divide(acc4, qm);
   }
-  store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
-  if (a.wire) {
-    const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
-    store_wire<XF, FULL>(a.wire, e0, mask, pre ? xl : xn);
-  }
-  if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
+  store_results<MODE, FULL, STATS, XF>(a, e0, mask, gbar, xl, xn, acc);
 }
 
 // ------------------------------------- batched vectors (stream counts known)
@@ -312,19 +334,14 @@ __device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned m
 #pragma unroll
     for (int r = 1; r < V::kG; ++r) s = s + v.g[r];
     gbar = divide(s, qg);
-    if constexpr (MODE == kModeAvg) {
-      store_f32<FULL, true>(a.gavg, e0, mask, gbar);
-      return;
-    }
-    if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
+    store_avg<MODE, FULL>(a, e0, mask, gbar);
+    if constexpr (MODE == kModeAvg) return;
   }
   f32x4 xl = v.x;
   if constexpr (MODE == kModeFused) {
-    f32x4 d = gbar;
-    if (a.wd != 0.0f) d = gbar + (a.wd * v.x);
-    const f32x4 m_new = (a.mu * v.m) + d;
-    xl = v.x - (a.lr * m_new);
-    store_f32<FULL, kNtParams>(a.m, e0, mask, m_new);
+    f32x4 m = v.m;
+    xl = sgd_momentum4(a, v.x, m, gbar);
+    store_f32<FULL, kNtParams>(a.m, e0, mask, m);
   }
   f32x4 xn = xl;
   if constexpr (V::kP > 0) {
@@ -333,12 +350,7 @@ __device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned m
     for (int i = 0; i < V::kP; ++i) acc4 = acc4 + received<XF>(v.s[i]);
     xn = divide(acc4, qm);
   }
-  store_f32<FULL, kNtParams>(a.x, e0, mask, xn);
-  if (a.wire) {
-    const bool pre = (MODE == kModeFused) && (a.flags & DASO_PACK_PRE_MERGE);
-    store_wire<XF, FULL>(a.wire, e0, mask, pre ? xl : xn);
-  }
-  if constexpr (STATS && MODE == kModeFused) accumulate(acc, gbar, xl, xn, mask);
+  store_results<MODE, FULL, STATS, XF>(a, e0, mask, gbar, xl, xn, acc);
 }
 
 // Whether an instance has compile-time stream counts (and so the batched path).
