@@ -36,7 +36,9 @@
  * Conventions for every entry point.
  *  - Buffers are device memory owned by the caller (the library allocates none of
  *    them).  fp32 buffers hold n floats, bf16 buffers hold n uint16 bit patterns.
- *  - Every device base pointer must be 16-byte aligned (DASO_EALIGN otherwise).
+ *  - Every device base pointer must be 16-byte aligned (DASO_EALIGN otherwise);
+ *    128-byte alignment (what hipMalloc returns) lets every wavefront access
+ *    whole cache lines and is the fast case.
  *  - Host pointer arrays (grads, stale) and bucket tables are read during the call
  *    only; the caller may free or reuse them as soon as the call returns.
  *  - Work is enqueued on `stream` (0 = the null stream) and runs asynchronously;
