@@ -75,7 +75,8 @@ extern "C" {
 
 /* status codes */
 #define DASO_OK 0
-#define DASO_EINVAL (-1)  /* null required pointer, bad count, S outside [0, DASO_MAX_S], buckets not a tiling of [0,n),
+#define DASO_EINVAL (-1)  /* null required pointer, bad count (n outside [0, DASO_MAX_N], g or P out of range),
+                             S outside [0, DASO_MAX_S], buckets not a tiling of [0,n),
                              a stream of another device */
 #define DASO_EALIGN (-2)  /* a device base pointer is not 16-byte aligned */
 #define DASO_EALIAS (-3)  /* an output overlaps an input other than in the allowed in-place pairs */
@@ -84,6 +85,7 @@ extern "C" {
 #define DASO_MAX_G 64     /* most replica gradients per call */
 #define DASO_MAX_P 64     /* most exchanged copies per call */
 #define DASO_MAX_S (1 << 20) /* largest staleness: 2S and 2S + P stay exact in binary32 */
+#define DASO_MAX_N ((int64_t)1 << 56) /* most elements per call (far beyond any memory; keeps byte spans in 64 bits) */
 
 /* flags of daso_sync_args */
 #define DASO_PACK_PRE_MERGE 1u /* pack xl (after the optimizer step, before Eq. (1)) instead of x' */

@@ -58,7 +58,7 @@ int check_buckets(const daso_bucket* b, int32_t nb, int64_t n) {
 }
 
 int check_local_avg(const float* const* grads, int32_t g, const float* out, int64_t n) {
-  if (n < 0 || g < 1 || g > DASO_MAX_G) return DASO_EINVAL;
+  if (n < 0 || n > DASO_MAX_N || g < 1 || g > DASO_MAX_G) return DASO_EINVAL;
   if (n == 0) return DASO_OK;
   int rc = check_ptr_table(reinterpret_cast<const void* const*>(grads), g);
   if (rc != DASO_OK) return rc;
@@ -70,7 +70,7 @@ int check_local_avg(const float* const* grads, int32_t g, const float* out, int6
 }
 
 int check_pack(const float* src, const uint16_t* wire, int64_t n) {
-  if (n < 0) return DASO_EINVAL;
+  if (n < 0 || n > DASO_MAX_N) return DASO_EINVAL;
   if (n == 0) return DASO_OK;
   int rc = check_out(src);
   if (rc != DASO_OK) return rc;
@@ -80,7 +80,7 @@ int check_pack(const float* src, const uint16_t* wire, int64_t n) {
 
 int check_merge(const float* params, const void* const* stale, int32_t P, const daso_bucket* buckets,
                 int32_t nbuckets, const void* wire, int64_t n, size_t esz) {
-  if (n < 0 || P < 0 || P > DASO_MAX_P) return DASO_EINVAL;
+  if (n < 0 || n > DASO_MAX_N || P < 0 || P > DASO_MAX_P) return DASO_EINVAL;
   if (n == 0) return DASO_OK;
   int rc = check_out(params);
   if (rc != DASO_OK) return rc;
@@ -100,7 +100,7 @@ int check_merge(const float* params, const void* const* stale, int32_t P, const 
 }
 
 int check_fused(const daso_sync_args& s, FusedView* view) {
-  if (s.n < 0 || s.g < 1 || s.g > DASO_MAX_G || s.P < 0 || s.P > DASO_MAX_P) return DASO_EINVAL;
+  if (s.n < 0 || s.n > DASO_MAX_N || s.g < 1 || s.g > DASO_MAX_G || s.P < 0 || s.P > DASO_MAX_P) return DASO_EINVAL;
   if ((s.flags & ~(DASO_PACK_PRE_MERGE | DASO_EXCHANGE_F32)) != 0) return DASO_EINVAL;
   const bool xf32 = (s.flags & DASO_EXCHANGE_F32) != 0;
   // the exchanged copies and the wire, in the exchange type

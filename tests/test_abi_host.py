@@ -210,6 +210,81 @@ def test_global_merge_f32_rejects(lib):
     assert f(A, st, 2, ok_b, 1, None, 0, None) == L.DASO_OK
 
 
+def test_element_count_limit(lib):
+    """n beyond DASO_MAX_N (2^56) is refused before any byte span is formed."""
+    _no_gpu()
+    big = (1 << 56) + 1
+    assert lib.daso_pack_bf16(A, A + 8 * MB, big, None) == L.DASO_EINVAL
+    assert lib.daso_local_avg(ptrs(A), 1, A + 8 * MB, big, None) == L.DASO_EINVAL
+    assert lib.daso_global_merge(A, ptrs(A + MB), 1, L.bucket_table([(0, big, 1)]), 1, None, big,
+                                 None) == L.DASO_EINVAL
+    a, keep = _args()
+    a.n = big
+    assert lib.daso_fused_sync_step(ctypes.byref(a), None) == L.DASO_EINVAL
+
+
+def _spans_overlap(p, nbytes, q, mbytes):
+    return p < q + mbytes and q < p + nbytes
+
+
+def _expected_fused(n, grads, stale, params, momentum, wire, grad_avg, stats, nb):
+    """The aliasing rule of daso_fused_sync_step, written from its header comment:
+    params, momentum, wire and stats overlap nothing else (inputs or outputs);
+    grad_avg overlaps no output and no copy, and of the gradients at most the one
+    buffer it equals exactly."""
+    ins = [(g, 4 * n) for g in grads] + [(s, 2 * n) for s in stale]
+    outs = [(params, 4 * n), (momentum, 4 * n)]
+    if wire:
+        outs.append((wire, 2 * n))
+    if stats:
+        outs.append((stats, 24 * nb))
+    for i, o in enumerate(outs):
+        if any(_spans_overlap(*o, *x) for x in outs[i + 1:] + ins):
+            return L.DASO_EALIAS
+    if grad_avg:
+        ga = (grad_avg, 4 * n)
+        if any(_spans_overlap(*ga, *o) for o in outs) or any(_spans_overlap(*ga, s, 2 * n) for s in stale):
+            return L.DASO_EALIAS
+        if any(g != grad_avg and _spans_overlap(*ga, g, 4 * n) for g in grads):
+            return L.DASO_EALIAS
+    return L.DASO_EHIP          # passes every check; with no GPU the launch then fails
+
+
+def test_fused_aliasing_rule_on_random_layouts(lib):
+    """Random buffer layouts in a small fake address range (so that overlaps are
+    frequent), every pointer aligned and the buckets valid: the status must be
+    exactly what the header's aliasing rule says."""
+    _no_gpu()
+    hypothesis = pytest.importorskip("hypothesis")
+    st = hypothesis.strategies
+
+    @hypothesis.settings(max_examples=400, deadline=None, derandomize=True)
+    @hypothesis.given(st.data())
+    def check(data):
+        n = data.draw(st.integers(1, 64)) * 4
+        g = data.draw(st.integers(1, 3))
+        P = data.draw(st.integers(0, 3))
+        slots = 48                                   # buffers start on a 16-byte grid of this many slots
+        addr = st.integers(0, slots).map(lambda k: A + 16 * k * 8)
+        grads = [data.draw(addr) for _ in range(g)]
+        stale = [data.draw(addr) for _ in range(P)]
+        params, momentum = data.draw(addr), data.draw(addr)
+        wire = data.draw(st.one_of(st.none(), addr))
+        grad_avg = data.draw(st.one_of(st.none(), addr, st.sampled_from(grads)))
+        stats = data.draw(st.one_of(st.none(), addr))
+        a = L.daso_sync_args()
+        keep = [ptrs(*grads), ptrs(*stale), L.bucket_table([(0, n, 1)])]
+        a.n, a.g, a.P = n, g, P
+        a.grads, a.stale = keep[0], keep[1]
+        a.params, a.momentum, a.wire, a.grad_avg, a.stats = params, momentum, wire, grad_avg, stats
+        a.buckets, a.nbuckets = keep[2], 1
+        a.lr, a.mu, a.weight_decay, a.flags = 0.1, 0.9, 0.0, 0
+        want = _expected_fused(n, grads, stale, params, momentum, wire, grad_avg, stats, 1)
+        assert lib.daso_fused_sync_step(ctypes.byref(a), None) == want
+
+    check()
+
+
 # ----------------------------------------------------------- bucket plan
 def test_plan_buckets_matches_the_workload_recipes(lib):
     """The library's layout planner reproduces the bucket tables of every
