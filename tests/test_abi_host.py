@@ -285,6 +285,44 @@ def test_fused_aliasing_rule_on_random_layouts(lib):
     check()
 
 
+def test_merge_and_local_avg_aliasing_rules_on_random_layouts(lib):
+    """As above for daso_global_merge (params and wire overlap neither each other
+    nor a copy) and daso_local_avg (out may be exactly one gradient buffer and
+    overlaps no other)."""
+    _no_gpu()
+    hypothesis = pytest.importorskip("hypothesis")
+    st = hypothesis.strategies
+
+    @hypothesis.settings(max_examples=300, deadline=None, derandomize=True)
+    @hypothesis.given(st.data())
+    def check(data):
+        n = data.draw(st.integers(1, 64)) * 4
+        addr = st.integers(0, 40).map(lambda k: A + 128 * k)
+        # merge
+        P = data.draw(st.integers(0, 4))
+        stale = [data.draw(addr) for _ in range(P)]
+        params = data.draw(addr)
+        wire = data.draw(st.one_of(st.none(), addr))
+        want = L.DASO_EHIP
+        if any(_spans_overlap(params, 4 * n, s_, 2 * n) for s_ in stale):
+            want = L.DASO_EALIAS
+        if wire and (_spans_overlap(wire, 2 * n, params, 4 * n)
+                     or any(_spans_overlap(wire, 2 * n, s_, 2 * n) for s_ in stale)):
+            want = L.DASO_EALIAS
+        got = lib.daso_global_merge(params, ptrs(*stale), P, L.bucket_table([(0, n, 2)]), 1, wire, n, None)
+        assert got == want
+        # local average
+        g = data.draw(st.integers(1, 4))
+        grads = [data.draw(addr) for _ in range(g)]
+        out = data.draw(st.one_of(addr, st.sampled_from(grads)))
+        want = L.DASO_EHIP
+        if any(gr != out and _spans_overlap(out, 4 * n, gr, 4 * n) for gr in grads):
+            want = L.DASO_EALIAS
+        assert lib.daso_local_avg(ptrs(*grads), g, out, n, None) == want
+
+    check()
+
+
 # ----------------------------------------------------------- bucket plan
 def test_plan_buckets_matches_the_workload_recipes(lib):
     """The library's layout planner reproduces the bucket tables of every
