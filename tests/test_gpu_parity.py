@@ -486,6 +486,7 @@ F32X_CASES = [
     (62, 33_333, 3, 5, 4, 1e-4, daso.DASO_PACK_PRE_MERGE),
     (63, 4097, 8, 32, 2, 0.0, 0),
     (64, 262_144, 4, 8, 1, 0.0, daso.DASO_PACK_PRE_MERGE),
+    (65, 600_001, 8, 32, 3, 0.0, 0),           # run-time-count instance over whole XCD run blocks
 ]
 
 
