@@ -515,6 +515,11 @@ __global__ __launch_bounds__(kBlock) void stats_kernel(const StepArgs a) {
   }
 }
 
+// Fused instances with compile-time stream counts for the node shapes: g = 4
+// or 8 replicas (the GPUs of a node) with P = 2 to 32 exchanged copies (the
+// nodes of a group), and the local step (P = 0).  Any other pair runs the
+// run-time-count instance, measured 3 to 4% slower for g = 8 and 22% for
+// g = 4, P = 32.
 template <bool STATS, typename F>
 auto dispatch_fused(const StepArgs& a, const F& f) {
   if (a.xf32) {
@@ -530,11 +535,26 @@ auto dispatch_fused(const StepArgs& a, const F& f) {
       default: break;
     }
   }
-  if (a.g == 4 && a.P == 2) return f.template run<kModeFused, 4, 2, STATS, false>();
-  if (a.g == 4 && a.P == 4) return f.template run<kModeFused, 4, 4, STATS, false>();
-  if (a.g == 4 && a.P == 8) return f.template run<kModeFused, 4, 8, STATS, false>();
-  if (a.g == 4 && a.P == 16) return f.template run<kModeFused, 4, 16, STATS, false>();
-  if (a.g == 8 && a.P == 32) return f.template run<kModeFused, 8, 32, STATS, false>();
+  if (a.g == 4) {
+    switch (a.P) {
+      case 2: return f.template run<kModeFused, 4, 2, STATS, false>();
+      case 4: return f.template run<kModeFused, 4, 4, STATS, false>();
+      case 8: return f.template run<kModeFused, 4, 8, STATS, false>();
+      case 16: return f.template run<kModeFused, 4, 16, STATS, false>();
+      case 32: return f.template run<kModeFused, 4, 32, STATS, false>();
+      default: break;
+    }
+  }
+  if (a.g == 8) {
+    switch (a.P) {
+      case 2: return f.template run<kModeFused, 8, 2, STATS, false>();
+      case 4: return f.template run<kModeFused, 8, 4, STATS, false>();
+      case 8: return f.template run<kModeFused, 8, 8, STATS, false>();
+      case 16: return f.template run<kModeFused, 8, 16, STATS, false>();
+      case 32: return f.template run<kModeFused, 8, 32, STATS, false>();
+      default: break;
+    }
+  }
   return f.template run<kModeFused, 0, -1, STATS, false>();
 }
 

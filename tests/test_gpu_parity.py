@@ -318,6 +318,20 @@ def test_fused_other_constants_and_large_S(case):
     compare_fused(got, want, f"fused constants {case}", gavg=True)
 
 
+@pytest.mark.parametrize("g,P", [(4, 32), (8, 2), (8, 4), (8, 8), (8, 16)])
+def test_fused_node_shapes(g, P):
+    """The compile-time instances for 4- and 8-GPU nodes (g) in groups of 2 to
+    32 nodes (P), over several XCD run blocks and a ragged tail."""
+    rng = np.random.default_rng(900 + 10 * g + P)
+    n = 700_001
+    bks = random_buckets(rng, n, 4)
+    inp = random_inputs(rng, n, g, P)
+    announce("fused node shape g=", g, "P=", P)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9, 1e-4)
+    got = run_fused(inp, bks, wd=1e-4, gavg="new")
+    compare_fused(got, want, f"node shape g={g} P={P}", gavg=True)
+
+
 @pytest.mark.parametrize("seed", [21, 22, 23])
 def test_fused_special_values(seed):
     """NaN, infinities, subnormals, the largest finite values and signed zeros
