@@ -517,12 +517,23 @@ __global__ __launch_bounds__(kBlock) void stats_kernel(const StepArgs a) {
 
 // Fused instances with compile-time stream counts for the node shapes: g = 4
 // or 8 replicas (the GPUs of a node) with P in {2, 4, 8, 16, 32} exchanged
-// copies (the nodes of a group), and the local step (P = 0).  Any other pair
-// runs the run-time-count instance, measured 4 to 7% slower on these shapes.
+// copies (the nodes of a group), bf16 or fp32, and the local step (P = 0).  Any
+// other pair runs the run-time-count instance, measured 4 to 7% slower on
+// these shapes with bf16 copies.
 template <bool STATS, typename F>
 auto dispatch_fused(const StepArgs& a, const F& f) {
   if (a.xf32) {
-    if (a.g == 4 && a.P == 8) return f.template run<kModeFused, 4, 8, STATS, true>();
+    if (a.g == 4 || a.g == 8) {
+      const bool g8 = a.g == 8;
+      switch (a.P) {
+        case 2: return g8 ? f.template run<kModeFused, 8, 2, STATS, true>() : f.template run<kModeFused, 4, 2, STATS, true>();
+        case 4: return g8 ? f.template run<kModeFused, 8, 4, STATS, true>() : f.template run<kModeFused, 4, 4, STATS, true>();
+        case 8: return g8 ? f.template run<kModeFused, 8, 8, STATS, true>() : f.template run<kModeFused, 4, 8, STATS, true>();
+        case 16: return g8 ? f.template run<kModeFused, 8, 16, STATS, true>() : f.template run<kModeFused, 4, 16, STATS, true>();
+        case 32: return g8 ? f.template run<kModeFused, 8, 32, STATS, true>() : f.template run<kModeFused, 4, 32, STATS, true>();
+        default: break;
+      }
+    }
     return f.template run<kModeFused, 0, -1, STATS, true>();
   }
   if (a.P == 0) {  // the local step of most cycling batches (no copies arrive)

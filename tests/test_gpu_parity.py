@@ -332,6 +332,21 @@ def test_fused_node_shapes(g, P):
     compare_fused(got, want, f"node shape g={g} P={P}", gavg=True)
 
 
+@pytest.mark.parametrize("g,P", [(4, 2), (4, 4), (4, 16), (4, 32), (8, 2), (8, 4), (8, 8), (8, 16)])
+def test_fused_node_shapes_f32_exchange(g, P):
+    """The fp32-exchange instances for the node shapes."""
+    rng = np.random.default_rng(950 + 10 * g + P)
+    n = 300_007
+    bks = random_buckets(rng, n, 3)
+    inp = random_inputs(rng, n, g, 0)
+    inp["stale"] = [(inp["params"] + (rng.standard_normal(n) * 1e-4).astype(F32)).astype(F32) for _ in range(P)]
+    announce("fused node shape, fp32 exchange, g=", g, "P=", P)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9,
+                             exchange="f32")
+    got = run_fused(inp, bks, gavg="new", f32=True)
+    compare_fused(got, want, f"node shape f32 g={g} P={P}", gavg=True)
+
+
 @pytest.mark.parametrize("seed", [21, 22, 23])
 def test_fused_special_values(seed):
     """NaN, infinities, subnormals, the largest finite values and signed zeros
