@@ -14,6 +14,13 @@ does and runs the matching library calls on this GPU's flat buffers:
   * DASO_ACT_RECV_BCAST: the caller overwrites the parameters with the state
     its node's group member merged (the local update step).
 
+With exchange="bf16" (the default) every exchange carries bf16 (Section 4:
+DASO compresses to bfloat16).  With exchange="cast_blocking" only the blocking
+exchanges are cast to bf16, while the non-blocking ones of the cycling phase
+send the parameters uncast in fp32 (Section 3: casting would only hold back a
+non-blocking send); self.wire is then the bf16 wire and self.wire_f32 the fp32
+one, and the copies handed to step() must be of the type that was sent.
+
 The exchanges themselves (the collectives) are the caller's: this module only
 orders the kernel calls.  Every computation runs in the library's kernels.
 """
@@ -29,14 +36,19 @@ from . import _lib as L
 class DasoSync:
     def __init__(self, schedule: "L.Schedule", params: torch.Tensor, momentum: torch.Tensor,
                  bucket_spans: Sequence[Tuple[int, int]], lr: float, mu: float, weight_decay: float = 0.0,
-                 stats: bool = False):
+                 stats: bool = False, exchange: str = "bf16"):
+        if exchange not in ("bf16", "cast_blocking"):
+            raise ValueError("exchange is 'bf16' or 'cast_blocking'")
         self.schedule = schedule
         self.params = params
         self.momentum = momentum
         self.spans = [(int(s), int(k)) for (s, k) in bucket_spans]
         self.lr, self.mu, self.wd = float(lr), float(mu), float(weight_decay)
+        self.exchange = exchange
         n = params.numel()
         self.wire = torch.empty(n, dtype=torch.int16, device=params.device)
+        self.wire_f32 = (torch.empty(n, dtype=torch.float32, device=params.device)
+                         if exchange == "cast_blocking" else None)
         self.stats = L.new_stats(len(self.spans), device=params.device) if stats else None
 
     def next_plan(self) -> Optional[dict]:
@@ -61,7 +73,12 @@ class DasoSync:
             raise ValueError("copies are passed exactly when the plan merges (DASO_ACT_MERGE)")
         stale = list(arrived) if merge else []
         S = plan["S"] if merge else 0
-        wire = self.wire if acts & (L.ACT_SEND | L.ACT_BLOCKING) else None
+        uncast = self.exchange == "cast_blocking" and plan["phase"] == L.PHASE_CYCLING
+        if uncast and any(c.dtype != torch.float32 for c in stale):
+            raise ValueError("with exchange='cast_blocking' the cycling phase's copies are fp32")
+        wire = None
+        if acts & (L.ACT_SEND | L.ACT_BLOCKING):
+            wire = self.wire_f32 if uncast else self.wire
         L.fused_sync_step(grads, self.params, self.momentum, stale, self._buckets(S), self.lr, self.mu, self.wd,
                           wire=wire, stats=self.stats)
 

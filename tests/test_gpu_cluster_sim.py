@@ -15,7 +15,10 @@ pytestmark = pytest.mark.gpu
 F32 = np.float32
 
 
-def test_simulated_cluster_matches_oracle():
+@pytest.mark.parametrize("exchange", ["bf16", "cast_blocking"])
+def test_simulated_cluster_matches_oracle(exchange):
+    """exchange="bf16": every exchange in bf16; "cast_blocking": bf16 for the
+    blocking exchanges only, fp32 for the non-blocking ones (Section 3)."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     nodes, g, n = 4, 4, 40_003
@@ -33,7 +36,7 @@ def test_simulated_cluster_matches_oracle():
 
     # GPU side
     syncs = [daso.DasoSync(daso.Schedule(**cfg), torch.from_numpy(x0[k].copy()).cuda(),
-                           torch.zeros(n, device="cuda"), spans, 0.1, 0.9) for k in range(nodes)]
+                           torch.zeros(n, device="cuda"), spans, 0.1, 0.9, exchange=exchange) for k in range(nodes)]
     sent = {}
     # oracle side
     xs = [x.copy() for x in x0]
@@ -50,11 +53,13 @@ def test_simulated_cluster_matches_oracle():
         kinds.add(acts)
         merge = bool(acts & OS.MERGE)
         S = ref["S"] if merge else 0
+        uncast = exchange == "cast_blocking" and ref["phase"] == OS.CYCLING
         bks = [(s, k, S) for (s, k) in spans]
         grads_dev = [[torch.from_numpy(a).cuda() for a in grads_all[t][k]] for k in range(nodes)]
         for k in range(nodes):
             syncs[k].step(ref, grads_dev[k], arrived=sent[t - S] if merge else None)
-            out = O.fused_sync_step(grads_all[t][k], xs[k], ms[k], sent_ref[t - S] if merge else [], bks, 0.1, 0.9)
+            out = O.fused_sync_step(grads_all[t][k], xs[k], ms[k], sent_ref[t - S] if merge else [], bks, 0.1, 0.9,
+                                    exchange="f32" if uncast else "bf16")
             xs[k], ms[k] = out["params"], out["momentum"]
             if acts & (OS.SEND | OS.BLOCKING):
                 wire_ref[k] = out["wire"]
@@ -65,7 +70,7 @@ def test_simulated_cluster_matches_oracle():
                 syncs[k].blocking_average(copies)
                 xs[k] = O.global_merge(xs[k], copies_ref, [(s, kk, 0) for (s, kk) in spans])[0]
         if acts & OS.SEND:
-            sent[t] = [s.wire.clone() for s in syncs]
+            sent[t] = [(s.wire_f32 if uncast else s.wire).clone() for s in syncs]
             sent_ref[t] = list(wire_ref)
         if ref["batch"] == nb - 1:
             for s in syncs:

@@ -187,3 +187,11 @@ def test_driver_checks_copies_against_the_plan():
         sync.step(no_merge, grads, arrived=[copy])
     with pytest.raises(ValueError):
         sync.step(merge, grads)
+    with pytest.raises(ValueError):
+        daso.DasoSync(daso.Schedule(1, 0, 0, 4, 1), x, torch.zeros(64), [(0, 64)], 0.1, 0.9, exchange="fp8")
+    # casting only the blocking exchanges: the cycling phase's copies must be fp32
+    sync32 = daso.DasoSync(daso.Schedule(1, 0, 0, 4, 1), x, torch.zeros(64), [(0, 64)], 0.1, 0.9,
+                           exchange="cast_blocking")
+    cycling_merge = {"actions": L.ACT_MERGE, "S": 1, "phase": L.PHASE_CYCLING}
+    with pytest.raises(ValueError):
+        sync32.step(cycling_merge, grads, arrived=[copy])
