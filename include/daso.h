@@ -11,8 +11,9 @@
  *
  *        x  <-  ( 2S * x_local + sum_{i=1..P} x_i ) / ( 2S + P )
  *
- * Parameters travel as bfloat16: they are cast while the send buffer is packed
- * and cast back on receipt (Section 3; Section 4 names bfloat16).
+ * Parameters travel as bfloat16 by default: they are cast while the send buffer
+ * is packed and cast back on receipt (Section 3; Section 4 names bfloat16).
+ * DASO_EXCHANGE_F32 and daso_global_merge_f32 cover an uncast fp32 exchange.
  *
  * This library runs that per-element arithmetic for one GPU's parameters, held
  * as flat buffers (all tensors of a model laid end to end) split into buckets,
@@ -28,7 +29,8 @@
  *     P == 0:  x' = xl
  *     P >  0:  a = (2S) * xl ; a = a + widen(stale_i[j]) (i = 1..P) ; x' = a / (2S+P)
  *     wire[j] = bf16_rne(x')   (or bf16_rne(xl) with DASO_PACK_PRE_MERGE)
- * widen(h) places the bf16 pattern h in the top half of a binary32 (exact).
+ * widen(h) places the bf16 pattern h in the top half of a binary32 (exact); with
+ * the fp32 exchange widen is the identity and the wire holds x' (or xl) itself.
  * bf16_rne rounds to nearest with ties to even; +-inf stay infinite, finite
  * values past the largest bfloat16 round to infinity, NaN becomes 0x7FC0.
  * Results are deterministic: the same inputs give the same bits on every call.
