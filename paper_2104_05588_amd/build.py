@@ -16,6 +16,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libdaso.so")
 CAPI_CLIENT_SRC = os.path.join(ROOT, "tests", "c", "fused_step_capi.c")
 CAPI_CLIENT = os.path.join(PKG, "fused_step_capi")  # next to libdaso.so (found through $ORIGIN)
+CAPI_CLUSTER_SRC = os.path.join(ROOT, "tests", "c", "daso_cluster_capi.c")
+CAPI_CLUSTER = os.path.join(PKG, "daso_cluster_capi")
 
 SOURCES = ["daso_kernels.hip", "daso_api.hip", "daso_host.cpp", "daso_schedule.cpp"]
 
@@ -60,16 +62,19 @@ def build(verbose: bool = False) -> str:
 
 
 def build_capi_client(verbose: bool = False) -> str:
-    """The plain C test client of the ABI (tests/c), linked against libdaso.so."""
-    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE, "-I", "/opt/rocm/include",
-           CAPI_CLIENT_SRC, "-o", CAPI_CLIENT, "-L", PKG, "-ldaso", "-L", "/opt/rocm/lib", "-lamdhip64",
-           "-Wl,-rpath,$ORIGIN", "-Wl,-rpath,/opt/rocm/lib"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"gcc failed with status {res.returncode}")
+    """The plain C test programs of the ABI (tests/c), linked against libdaso.so."""
+    for src, exe in ((CAPI_CLIENT_SRC, CAPI_CLIENT), (CAPI_CLUSTER_SRC, CAPI_CLUSTER)):
+        if not os.path.exists(src):
+            continue
+        cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE, "-I", "/opt/rocm/include",
+               src, "-o", exe, "-L", PKG, "-ldaso", "-L", "/opt/rocm/lib", "-lamdhip64",
+               "-Wl,-rpath,$ORIGIN", "-Wl,-rpath,/opt/rocm/lib"]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError(f"gcc failed with status {res.returncode}")
     return CAPI_CLIENT
 
 
