@@ -82,6 +82,21 @@ class DasoSync:
         L.fused_sync_step(grads, self.params, self.momentum, stale, self._buckets(S), self.lr, self.mu, self.wd,
                           wire=wire, stats=self.stats)
 
+    def fast_forward(self, batches: int, losses: Sequence[float]) -> None:
+        """Resume a checkpointed run: bring this object's fresh controller to
+        the point after `batches` batches.  The controller depends only on its
+        configuration and the epoch losses, so replaying its plans, with the
+        loss of every epoch completed within those batches, restores it.  The
+        parameters, momentum and the copies still in flight are the caller's to
+        restore."""
+        nb = self.schedule.config.batches_per_epoch
+        for _ in range(int(batches)):
+            plan = self.schedule.next_batch()
+            if plan is None:
+                raise ValueError("the schedule has fewer batches than that")
+            if plan["batch"] == nb - 1:
+                self.schedule.end_epoch(losses[plan["epoch"]])
+
     def blocking_average(self, copies: Sequence[torch.Tensor]) -> None:
         """Finish a blocking synchronisation: the parameters become the plain
         average (Eq. (1) with S = 0) of the group's P exchanged copies."""

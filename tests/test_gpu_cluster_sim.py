@@ -84,3 +84,65 @@ def test_simulated_cluster_matches_oracle(exchange):
     # the cluster stays together: after the blocking cool-down every node holds the same state
     for k in range(1, nodes):
         assert np.array_equal(xs[k], xs[0])
+
+
+def test_checkpoint_and_resume_reproduce_the_uninterrupted_run():
+    """Stop a simulated cluster after 20 of 36 batches (mid-epoch, with copies in
+    flight), keep params, momentum and the sent copies, resume in fresh objects
+    whose controllers are fast-forwarded with the losses seen so far: the final
+    state equals the uninterrupted run's bit for bit."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nodes, g, n = 3, 2, 20_011
+    spans = [(0, 9_001), (9_001, n - 9_001)]
+    E, nb = 6, 6
+    cfg = dict(total_epochs=E, warmup_epochs=1, cooldown_epochs=1, batches_per_epoch=nb, B_init=4,
+               W_init=2, group_count=1, local_rank=0, patience=1, plateau_rel_tol=0.0)
+    losses = [1.0, 0.9, 0.9, 0.9, 0.8, 0.8]
+    rng = np.random.default_rng(77)
+    x0 = [(rng.standard_normal(n) * 0.02).astype(F32) for _ in range(nodes)]
+    grads = [[[torch.from_numpy((rng.standard_normal(n) * 1e-3).astype(F32)).cuda() for _ in range(g)]
+              for _ in range(nodes)] for _ in range(E * nb)]
+
+    def make(params, momentum):
+        return [daso.DasoSync(daso.Schedule(**cfg), params[k], momentum[k], spans, 0.1, 0.9) for k in range(nodes)]
+
+    def run(syncs, sent, first, last):
+        for t in range(first, last):
+            plan = syncs[0].next_plan()
+            for s in syncs[1:]:
+                assert s.next_plan() == plan
+            acts = plan["actions"]
+            merge = bool(acts & daso.ACT_MERGE)
+            for k in range(nodes):
+                syncs[k].step(plan, grads[t][k], arrived=sent[t - plan["S"]] if merge else None)
+            if acts & daso.ACT_BLOCKING:
+                copies = [s.wire.clone() for s in syncs]
+                for s in syncs:
+                    s.blocking_average(copies)
+            if acts & daso.ACT_SEND:
+                sent[t] = [s.wire.clone() for s in syncs]
+            if plan["batch"] == nb - 1:
+                for s in syncs:
+                    s.end_epoch(losses[plan["epoch"]])
+
+    print("[case] checkpoint and resume after 20 of 36 batches", flush=True)
+    # the uninterrupted run
+    whole = make([torch.from_numpy(x.copy()).cuda() for x in x0], [torch.zeros(n, device="cuda") for _ in x0])
+    run(whole, {}, 0, E * nb)
+    # the interrupted one: checkpoint after batch 20, resume in fresh objects
+    part = make([torch.from_numpy(x.copy()).cuda() for x in x0], [torch.zeros(n, device="cuda") for _ in x0])
+    sent = {}
+    run(part, sent, 0, 20)
+    torch.cuda.synchronize()
+    ckpt = ([s.params.cpu().clone() for s in part], [s.momentum.cpu().clone() for s in part],
+            {t: [c.cpu().clone() for c in cs] for t, cs in sent.items()})
+    del part, sent
+    resumed = make([p.cuda() for p in ckpt[0]], [m.cuda() for m in ckpt[1]])
+    for s in resumed:
+        s.fast_forward(20, losses)
+    run(resumed, {t: [c.cuda() for c in cs] for t, cs in ckpt[2].items()}, 20, E * nb)
+    torch.cuda.synchronize()
+    for a, b in zip(whole, resumed):
+        assert torch.equal(a.params.view(torch.int32), b.params.view(torch.int32))
+        assert torch.equal(a.momentum.view(torch.int32), b.momentum.view(torch.int32))

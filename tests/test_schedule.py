@@ -195,3 +195,27 @@ def test_driver_checks_copies_against_the_plan():
     cycling_merge = {"actions": L.ACT_MERGE, "S": 1, "phase": L.PHASE_CYCLING}
     with pytest.raises(ValueError):
         sync32.step(cycling_merge, grads, arrived=[copy])
+
+
+def test_fast_forward_restores_the_controller():
+    """A fresh controller fast-forwarded through k batches with the losses seen
+    so far plans the remaining batches exactly as the original one."""
+    import torch
+    import paper_2104_05588_amd as daso
+    E, nb = 7, 5
+    losses = [1.0, 0.9, 0.9, 0.95, 0.7, 0.7, 0.6]
+    kw = dict(total_epochs=E, warmup_epochs=1, cooldown_epochs=1, batches_per_epoch=nb, B_init=4,
+              group_count=2, local_rank=1, patience=1)
+    want = _native_plans(daso.Schedule(**kw), losses, nb)
+    for k in (0, 1, 4, 5, 13, 34, E * nb):
+        sync = daso.DasoSync(daso.Schedule(**kw), torch.zeros(8), torch.zeros(8), [(0, 8)], 0.1, 0.9)
+        sync.fast_forward(k, losses)
+        rest = []
+        while (p := sync.next_plan()) is not None:
+            rest.append(p)
+            if p["batch"] == nb - 1:
+                sync.end_epoch(losses[p["epoch"]])
+        assert rest == want[k:], k
+    with pytest.raises(ValueError):
+        daso.DasoSync(daso.Schedule(**kw), torch.zeros(8), torch.zeros(8), [(0, 8)], 0.1, 0.9).fast_forward(
+            E * nb + 1, losses)
