@@ -332,6 +332,37 @@ def test_fused_node_shapes(g, P):
     compare_fused(got, want, f"node shape g={g} P={P}", gavg=True)
 
 
+@pytest.mark.parametrize("g,P", [(3, 12), (8, 12), (5, 8), (7, 16), (2, 9), (1, 0), (6, 0), (8, 3)])
+def test_fused_other_counts(g, P):
+    """Counts between the node shapes: the instances bounded by 4 or 8 replicas
+    and 8 or 16 copies (missing streams skipped), and the run-time-count one."""
+    rng = np.random.default_rng(970 + 10 * g + P)
+    n = 300_007
+    bks = random_buckets(rng, n, 3)
+    inp = random_inputs(rng, n, g, P)
+    announce("fused other counts g=", g, "P=", P)
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9, 1e-4)
+    got = run_fused(inp, bks, wd=1e-4, gavg="new")
+    compare_fused(got, want, f"other counts g={g} P={P}", gavg=True)
+
+
+@pytest.mark.parametrize("P", [9, 12, 16, 33])
+def test_global_merge_other_counts(P):
+    rng = np.random.default_rng(990 + P)
+    n = 200_003
+    bks = random_buckets(rng, n, 3)
+    x = (rng.standard_normal(n) * 0.02).astype(F32)
+    st = [O.bf16_rne(x + (rng.standard_normal(n) * 1e-4).astype(F32)) for _ in range(P)]
+    announce("global_merge other counts P=", P)
+    want, wire_want = O.global_merge(x, st, bks, pack=True)
+    xd = dev_f32(x)
+    wd = torch.empty(n, dtype=torch.int16, device="cuda")
+    daso.global_merge(xd, [dev_bf16(s_) for s_ in st], bks, wd)
+    torch.cuda.synchronize()
+    check_f32(host_f32(xd), want, f"merge P={P}")
+    check_u16(host_u16(wd), wire_want, f"merge wire P={P}")
+
+
 @pytest.mark.parametrize("g,P", [(4, 2), (4, 4), (4, 16), (4, 32), (8, 2), (8, 4), (8, 8), (8, 16)])
 def test_fused_node_shapes_f32_exchange(g, P):
     """The fp32-exchange instances for the node shapes."""
