@@ -99,9 +99,18 @@ def status_string(status: int) -> str:
 
 
 # ------------------------------------------------------------- marshalling
+# torch's raw getter for the current stream's handle costs about 0.1 us per
+# call against about 3 us for torch.cuda.current_stream(), which builds a
+# Stream object; the public route serves a torch without it.
+_current_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream_handle(stream: Optional[torch.cuda.Stream]) -> ctypes.c_void_p:
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return ctypes.c_void_p(s.cuda_stream)
+    if stream is not None:
+        return ctypes.c_void_p(stream.cuda_stream)
+    if _current_raw_stream is not None:
+        return ctypes.c_void_p(_current_raw_stream(torch.cuda.current_device()))
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
 def _ptr(t: Optional[torch.Tensor], dtypes: Tuple[torch.dtype, ...], n: int, what: str) -> Optional[int]:

@@ -23,14 +23,15 @@ using daso::TileBucket;
 using daso::TilePartial;
 
 // ---------------------------------------------------------------- workspace
-// Per (device, stream): the per-tile statistics partials of a fused launch.
-// Allocated on first use and replaced by one at least twice as large when a
-// larger launch needs it.  A replaced buffer is never freed: launches already
-// queued, and graphs captured earlier, may still use it; the doubling keeps the
-// total within twice the largest buffer.  Every launch writes each partial it
-// later reads, so the contents never need clearing.  A call holds the entry's
-// lock from choosing the buffer until its last launch is queued, so that two
-// host threads sharing a stream cannot queue one call's step between the other
+// Per (device, stream): the per-tile statistics partials of a fused launch,
+// followed by the launch's table of bucket tile ranges.  Allocated on first use
+// and replaced by one at least twice as large when a larger launch needs it.  A
+// replaced buffer is never freed: launches already queued, and graphs captured
+// earlier, may still use it; the doubling keeps the total within twice the
+// largest buffer.  Every launch writes each partial and table entry it later
+// reads, so the contents never need clearing.  A call holds the entry's lock
+// from choosing the buffer until its last launch is queued, so that two host
+// threads sharing a stream cannot queue one call's step between the other
 // call's step and its statistics pass.
 struct Workspace {
   std::mutex mu;
@@ -126,9 +127,11 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   if (with_stats) {
     Workspace& w = workspace_entry(dev, stream);
     hold = std::unique_lock<std::mutex>(w.mu);
-    const int rc = reserve(w, static_cast<size_t>(max_tiles) * sizeof(TilePartial));
+    const size_t table_at = static_cast<size_t>(max_tiles) * sizeof(TilePartial);
+    const int rc = reserve(w, table_at + (daso::kLaunchBuckets + 1) * sizeof(int32_t));
     if (rc != DASO_OK) return rc;
     a.partials = static_cast<TilePartial*>(w.ptr);
+    a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(w.ptr) + table_at);
   }
   for (const auto& gr : groups) {
     fill_group(a, b, gr, tile);

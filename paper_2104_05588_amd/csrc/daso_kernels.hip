@@ -464,6 +464,11 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   const Divisor qg = make_divisor((G > 0) ? G : a.g);
   const int w0 = a.xcd_run > 1 ? xcd_runs(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), a.xcd_run)
                                : static_cast<int>(blockIdx.x);
+  if constexpr (STATS && MODE == kModeFused) {
+    // the bucket ranges for stats_kernel (the grid has at least one workgroup)
+    const int k = static_cast<int>(threadIdx.x);
+    if (blockIdx.x == 0 && k <= a.nb) a.tile_table[k] = k < a.nb ? a.b[k].first_tile : a.ntiles;
+  }
   for (int64_t t = w0; t < a.ntiles; t += gridDim.x) {
     const int tile = static_cast<int>(t);
     // bucket owning this tile: the last one whose first tile is <= tile
@@ -497,11 +502,12 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
 // Statistics of one launch: workgroup i sums the tile partials of bucket i in
 // tile order (a fixed assignment and reduction tree, so the result does not
 // depend on timing).  Runs after step_kernel on the same stream, which makes
-// every partial visible without any fence inside step_kernel.
-__global__ __launch_bounds__(kBlock) void stats_kernel(const StepArgs a) {
+// every partial, and the tile table, visible without any fence inside
+// step_kernel.
+__global__ __launch_bounds__(kBlock) void stats_kernel(const StatsArgs a) {
   const int i = static_cast<int>(blockIdx.x);
-  const int t0 = a.b[i].first_tile;
-  const int t1 = (i + 1 < a.nb) ? a.b[i + 1].first_tile : a.ntiles;
+  const int t0 = a.tile_table[i];
+  const int t1 = a.tile_table[i + 1];
   Acc64 v = {0.0, 0.0, 0};
   // The kernel is latency-bound: each thread issues the loads of up to 16
   // partials (about 12 for a 25 MiB bucket of 2048-element tiles) before it
@@ -650,7 +656,9 @@ struct Launcher {
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&step_kernel<MODE, G, PP, STATS, XF>),
                                          dim3(a.ntiles), dim3(kBlock), args, 0, stream);
     if (e != hipSuccess || !STATS) return e;
-    return hipLaunchKernel(reinterpret_cast<const void*>(&stats_kernel), dim3(a.nb), dim3(kBlock), args, 0, stream);
+    StatsArgs sa = {a.partials, a.tile_table, a.stats, a.nb};
+    void* sargs[] = {&sa};
+    return hipLaunchKernel(reinterpret_cast<const void*>(&stats_kernel), dim3(a.nb), dim3(kBlock), sargs, 0, stream);
   }
 };
 

@@ -66,6 +66,8 @@ struct StepArgs {
   void* wire;            // packed output (bf16, or fp32 when xf32) or nullptr
   float* gavg;           // local average output or nullptr
   TilePartial* partials; // per-tile partials (stats only)
+  int32_t* tile_table;   // (stats only) nb + 1 entries written by workgroup 0 for stats_kernel:
+                         // the first tile of each bucket, then ntiles
   daso_bucket_stats* stats;  // per-bucket outputs (stats only), already offset to this launch
   int32_t g;
   int32_t P;
@@ -78,6 +80,16 @@ struct StepArgs {
   int32_t xcd_run;       // > 1: each XCD takes runs of this many consecutive tiles
   int32_t xf32;          // nonzero: fp32 exchange (stale copies and wire are fp32)
   TileBucket b[kLaunchBuckets];
+};
+
+// Arguments of stats_kernel, kept to a few pointers: the host cost of a launch
+// grows with the size of its arguments (about 2.7 us with 16 bytes, 4 us with
+// 2.7 KB on MI355X), and the bucket ranges it needs are in tile_table.
+struct StatsArgs {
+  const TilePartial* partials;
+  const int32_t* tile_table;
+  daso_bucket_stats* stats;
+  int32_t nb;
 };
 
 // Tiles lie on one grid of `tile` elements counted from element 0, so that a

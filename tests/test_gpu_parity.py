@@ -418,6 +418,18 @@ def test_fused_empty_buckets_and_many_launches():
     assert got["stats"][-1] == (0.0, 0.0, 0) and got["stats"][-2] == (0.0, 0.0, 0)
 
 
+def test_binding_launches_on_the_current_stream():
+    """With no stream given, the binding passes torch's current stream: the
+    default one, or the one a `torch.cuda.stream` context selects."""
+    from paper_2104_05588_amd import _lib as L
+    announce("binding stream handle")
+    side = torch.cuda.Stream()
+    assert (L._stream_handle(None).value or 0) == torch.cuda.current_stream().cuda_stream
+    with torch.cuda.stream(side):
+        assert L._stream_handle(None).value == side.cuda_stream
+    assert L._stream_handle(side).value == side.cuda_stream
+
+
 def test_fused_is_deterministic_and_stream_ordered():
     w = R.workload("resnet18")
     inp = Gen.host_inputs(w)
