@@ -54,8 +54,9 @@
  *    buffers are untouched.  daso_status_string names the status.
  *  - Calls may be made from several host threads.  Fused steps with statistics
  *    share one small per-(device, stream) workspace (24 bytes per tile of 1024
- *    or 2048 parameters) that the library allocates on first use, replaces by a larger
- *    one when a larger call needs it, and never frees before the process ends;
+ *    or 2048 parameters, plus a 260-byte table of bucket ranges) that the
+ *    library allocates on first use (at least 1 MiB), replaces by a larger one
+ *    when a larger call needs it, and never frees before the process ends;
  *    calls on one stream are ordered by that stream, and threads may share a
  *    stream (each call queues its kernels together).  A call that allocates
  *    cannot be captured into a HIP graph: make one call of the largest size on
