@@ -576,6 +576,39 @@ def test_fused_f32_exchange(case):
     compare_fused(got, want, f"fused f32 {case}", gavg=True)
 
 
+def test_fused_seeded_sweep_over_the_argument_space():
+    """Seeded random draws over every argument at once: replica and copy counts
+    that select the exact, bounded and run-time-count instances, both exchange
+    types, the pre-merge pack flag, the wire, grad_avg and statistics each on or
+    off, weight decay, S from 0 to 1000, and 1 to 8 buckets in any order over
+    sizes that span several tiles with ragged tails."""
+    rng = np.random.default_rng(2104_05588)
+    for case in range(64):
+        g = int(rng.choice([1, 2, 3, 4, 4, 5, 8, 8, 12, 16]))
+        P = int(rng.choice([0, 1, 2, 3, 4, 6, 8, 8, 12, 16, 20, 32, 40]))
+        f32 = bool(rng.random() < 0.3)
+        n = int(rng.integers(1, 70_000))
+        nb = int(rng.integers(1, 9))
+        flags = daso.DASO_PACK_PRE_MERGE if rng.random() < 0.25 else 0
+        wd = float(rng.choice([0.0, 1e-4]))
+        lr, mu = float(rng.choice([0.1, 0.05])), float(rng.choice([0.9, 0.0]))
+        wire = bool(rng.random() < 0.8)
+        stats = bool(rng.random() < 0.7)
+        gavg = str(rng.choice(["none", "new", "alias"]))
+        bks = random_buckets(rng, n, nb, (0, 1, 2, 3, 4, 7, 1000))
+        inp = random_inputs(rng, n, g, 0 if f32 else P)
+        if f32:
+            inp["stale"] = [(inp["params"] + (rng.standard_normal(n) * 1e-4).astype(F32)).astype(F32)
+                            for _ in range(P)]
+        what = f"sweep case {case}: n={n} g={g} P={P} f32={f32} buckets={len(bks)} flags={flags} " \
+               f"wire={wire} stats={stats} gavg={gavg} wd={wd} lr={lr} mu={mu}"
+        announce(what)
+        want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, lr, mu, wd,
+                                 flags, exchange="f32" if f32 else "bf16")
+        got = run_fused(inp, bks, lr=lr, mu=mu, wd=wd, flags=flags, wire=wire, gavg=gavg, stats=stats, f32=f32)
+        compare_fused(got, want, what, wire=wire, gavg=gavg != "none", stats=stats)
+
+
 # ----------------------------------------------------------- edge cases
 def test_empty_inputs_launch_nothing():
     announce("n = 0 on every entry point")
