@@ -103,6 +103,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
+    ap.add_argument("--node-shapes", action="store_true",
+                    help="time every node shape (g = 4 or 8 replicas, P = 0 to 32 copies, bf16 and fp32 "
+                         "exchange) on the resnet50-shaped parameter set instead of the one workload")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -131,6 +134,9 @@ def main() -> int:
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": nbytes, "dispatches": args.steps}), flush=True)
         return 0
+
+    if args.node_shapes:
+        return node_shapes(args, torch, daso, Gen, R)
 
     w = R.workload(args.workload)
     n = w.n
@@ -284,6 +290,57 @@ def main() -> int:
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
     print(json.dumps(out), flush=True)
+    return 0
+
+
+def node_shapes(args, torch, daso, Gen, R) -> int:
+    """Per-call time of the fused step for every node shape the library has a
+    compile-time instance for: g = 4 or 8 replicas (the GPUs of a node) and
+    P = 0, 2, 4, 8, 16 or 32 exchanged copies (the nodes of a group), with the
+    bf16 exchange and, for P > 0, the fp32 one; resnet50-shaped parameter set,
+    wire and statistics on, K calls between one pair of HIP events after W
+    warm-up calls.  Prints one JSON line."""
+    import dataclasses
+    base = R.workload("resnet50")
+    w = dataclasses.replace(base, g=8, P=32)
+    n = w.n
+    inp = Gen.device_inputs(w)
+    bks = [(b.start, b.numel, b.S) for b in w.buckets]
+    stale32 = [t.view(torch.bfloat16).float() for t in inp["stale"]]
+    wire16 = torch.empty(n, dtype=torch.int16, device="cuda")
+    wire32 = torch.empty(n, dtype=torch.float32, device="cuda")
+    stats = daso.new_stats(len(bks))
+    stream = torch.cuda.current_stream()
+    shapes = []
+    for exchange in ("bf16", "fp32"):
+        for g in (4, 8):
+            for P in (0, 2, 4, 8, 16, 32):
+                if exchange == "fp32" and P == 0:
+                    continue
+                f32 = exchange == "fp32"
+                step = daso.FusedStep(inp["grads"][:g], inp["params"], inp["momentum"],
+                                      (stale32 if f32 else inp["stale"])[:P], bks, w.lr, w.mu, w.wd,
+                                      wire=wire32 if f32 else wire16, stats=stats)
+                for _ in range(args.warmup):
+                    step()
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for _ in range(args.steps):
+                    step()
+                b.record(stream)
+                b.synchronize()
+                us = a.elapsed_time(b) * 1e3 / args.steps
+                bpp = 4 * g + 4 * P + 20 if f32 else R.algorithmic_bytes_per_param(g, P)
+                gbps = n * bpp / (us * 1e-6) / 1e9
+                shapes.append({"exchange": exchange, "g": g, "P": P, "us_per_call": us,
+                               "algorithmic_bytes_per_param": bpp, "GBps": gbps, "frac": gbps / PEAK_HBM_GBPS})
+                print(f"[shape] {exchange} g={g} P={P}: {us:.1f} us, {100 * gbps / PEAK_HBM_GBPS:.1f}% of peak",
+                      file=sys.stderr, flush=True)
+                del step
+    print(json.dumps({"node_shapes": shapes, "workload": f"{base.name}-shaped parameter set", "params": n,
+                      "buckets": len(bks), "steps": args.steps, "warmup": args.warmup,
+                      "peak_GBps": PEAK_HBM_GBPS}), flush=True)
     return 0
 
 

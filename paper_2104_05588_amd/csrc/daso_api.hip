@@ -121,8 +121,10 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   if (mode == daso::kModeAvg) streams = a.g + 1;
   if (mode == daso::kModeMerge) streams = a.P + 2 + (a.wire ? 1 : 0);
   if (mode == daso::kModeFused) streams = a.g + a.P + 4 + (a.wire ? 1 : 0) + (a.gavg ? 1 : 0);
-  a.xcd_run = streams >= daso::kXcdRunManyStreams ? daso::kXcdRunMany
-              : streams >= daso::kXcdRunMidStreams ? daso::kXcdRunMid : 1;
+  a.xcd_run = 1;
+  if (streams >= daso::kXcdRunManyStreams) a.xcd_run = daso::kXcdRunMany;
+  else if (streams >= daso::kXcdRunMidStreams) a.xcd_run = daso::kXcdRunMid;
+  else if (mode == daso::kModeFused && !a.xf32 && streams >= daso::kXcdRunFusedStreams) a.xcd_run = daso::kXcdRunMid;
   std::unique_lock<std::mutex> hold;
   if (with_stats) {
     Workspace& w = workspace_entry(dev, stream);
