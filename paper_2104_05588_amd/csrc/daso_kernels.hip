@@ -538,9 +538,9 @@ __global__ __launch_bounds__(kBlock) void stats_kernel(const StatsArgs a) {
 
 // Fused instances with compile-time stream counts for the node shapes: g = 4
 // or 8 replicas (the GPUs of a node) with P in {2, 4, 8, 16, 32} exchanged
-// copies (the nodes of a group), bf16 or fp32, and the local step (P = 0).  Any
-// other pair runs the run-time-count instance, measured 4 to 7% slower on
-// these shapes with bf16 copies.
+// copies (the nodes of a group), bf16 or fp32, and the local step (P = 0).
+// Other pairs run an instance with bounded counts (below) or the run-time-count
+// instance, which measured 3 to 7% slower than exact ones on the node shapes.
 template <bool STATS, typename F>
 auto dispatch_fused(const StepArgs& a, const F& f) {
   if (a.xf32) {
@@ -587,9 +587,9 @@ auto dispatch_fused(const StepArgs& a, const F& f) {
     }
   }
   // other counts up to 8 replicas and 16 copies: instances bounded by 4 or 8
-  // and 8 or 16 streams, the missing ones skipped (measured 3 to 8% faster than
-  // the run-time-count instance there; slower beyond 16 copies, and for g = 8
-  // with fewer than 8 copies)
+  // and 8 or 16 streams, the missing ones skipped (measured 4 to 7% faster than
+  // the run-time-count instance there; slower beyond 16 copies, and no faster
+  // for g = 8 with fewer than 8 copies)
   if (a.g <= 4 && a.P <= 16) {
     if (a.P <= 8) return f.template run<kModeFused, -4, -8, STATS, false>();
     return f.template run<kModeFused, -4, -16, STATS, false>();

@@ -32,12 +32,13 @@ constexpr bool kNtParams = DASO_NT_PARAMS != 0;  // non-temporal access to param
 constexpr int kGenericIters = 2;                 // vectors per thread for runtime stream counts
 constexpr int kLaunchBuckets = 64;
 // Tile order across the 8 XCDs: workgroups go to the XCDs in turn, and a
-// launch runs faster when each XCD takes runs of consecutive tiles (measured
-// on several MI355X: runs of 32 tiles +4 to 5% with 45 streams; runs of 16 +2
-// to 5% with 25, and +1.8 to 3.5% for the fused step with bf16 copies and 13
-// to 17 streams, the resnet50-shaped one included, never slower from 9; the
-// separate entry points and the fp32 exchange below 20 streams are within
-// about 1% either way and keep plain order).
+// launch runs faster when each XCD takes runs of consecutive tiles.  Measured
+// against plain order on several MI355X: runs of 32 tiles +4 to 5% with 45
+// streams; runs of 16 between -2.3% and +5.5% with 25 (three boxes), and +0.3
+// to +3.5% for the fused step with bf16 copies and 9 to 17 streams (the
+// resnet50-shaped one +0.3 to +2.7% on six boxes); the separate entry points
+// and the fp32 exchange below 20 streams move by about 1% either way and keep
+// plain order.
 constexpr int kXcdRunFusedStreams = 9;  // fused step, bf16 copies: runs of kXcdRunMid tiles from here
 constexpr int kXcdRunMidStreams = 20;   // any launch: runs of kXcdRunMid tiles from here
 constexpr int kXcdRunMid = 16;
