@@ -124,7 +124,8 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   a.xcd_run = 1;
   if (streams >= daso::kXcdRunManyStreams) a.xcd_run = daso::kXcdRunMany;
   else if (streams >= daso::kXcdRunMidStreams) a.xcd_run = daso::kXcdRunMid;
-  else if (mode == daso::kModeFused && !a.xf32 && streams >= daso::kXcdRunFusedStreams) a.xcd_run = daso::kXcdRunMid;
+  else if (mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams)
+    a.xcd_run = static_cast<int32_t>(std::max<int64_t>(1, daso::kXcdRunFusedElems / tile));
   std::unique_lock<std::mutex> hold;
   if (with_stats) {
     Workspace& w = workspace_entry(dev, stream);

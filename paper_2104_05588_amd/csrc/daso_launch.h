@@ -34,12 +34,14 @@ constexpr int kLaunchBuckets = 64;
 // Tile order across the 8 XCDs: workgroups go to the XCDs in turn, and a
 // launch runs faster when each XCD takes runs of consecutive tiles.  Measured
 // against plain order on several MI355X: runs of 32 tiles +4 to 5% with 45
-// streams; runs of 16 between -2.3% and +5.5% with 25 (three boxes), and +0.3
-// to +3.5% for the fused step with bf16 copies and 9 to 17 streams (the
-// resnet50-shaped one +0.3 to +2.7% on six boxes); the separate entry points
-// and the fp32 exchange below 20 streams move by about 1% either way and keep
-// plain order.
-constexpr int kXcdRunFusedStreams = 9;  // fused step, bf16 copies: runs of kXcdRunMid tiles from here
+// streams; runs of 16 between -2.3% and +5.5% with 25 (three boxes).  Below 20
+// streams the fused step is fastest with runs of 32K elements, 128 KB of each
+// fp32 stream (16 tiles of 2048 elements, 32 of 1024): the resnet50-shaped
+// step +0.3 to +2.7% on six boxes; fp32 exchange with 1024-element tiles +1
+// to +8%.  The separate entry points move by about 1% either way and keep
+// plain order there.
+constexpr int kXcdRunFusedStreams = 9;        // fused step: runs of kXcdRunFusedElems from here
+constexpr int64_t kXcdRunFusedElems = 32768;  // elements per run (a multiple of every tile)
 constexpr int kXcdRunMidStreams = 20;   // any launch: runs of kXcdRunMid tiles from here
 constexpr int kXcdRunMid = 16;
 constexpr int kXcdRunManyStreams = 32;  // any launch: runs of kXcdRunMany tiles from here

@@ -365,9 +365,10 @@ def test_global_merge_other_counts(P):
 
 @pytest.mark.parametrize("g,P", [(4, 2), (4, 4), (4, 16), (4, 32), (8, 2), (8, 4), (8, 8), (8, 16)])
 def test_fused_node_shapes_f32_exchange(g, P):
-    """The fp32-exchange instances for the node shapes."""
+    """The fp32-exchange instances for the node shapes, over several XCD run
+    blocks and a ragged tail."""
     rng = np.random.default_rng(950 + 10 * g + P)
-    n = 300_007
+    n = 700_007
     bks = random_buckets(rng, n, 3)
     inp = random_inputs(rng, n, g, 0)
     inp["stale"] = [(inp["params"] + (rng.standard_normal(n) * 1e-4).astype(F32)).astype(F32) for _ in range(P)]
