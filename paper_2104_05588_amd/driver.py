@@ -90,6 +90,11 @@ class DasoSync:
         parameters, momentum and the copies still in flight are the caller's to
         restore."""
         nb = self.schedule.config.batches_per_epoch
+        if int(batches) < 0:
+            raise ValueError("batches must be >= 0")
+        if len(losses) < int(batches) // nb:
+            raise ValueError(f"{int(batches)} batches complete {int(batches) // nb} epochs, "
+                             f"but only {len(losses)} epoch losses were given")
         for _ in range(int(batches)):
             plan = self.schedule.next_batch()
             if plan is None:

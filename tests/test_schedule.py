@@ -219,3 +219,9 @@ def test_fast_forward_restores_the_controller():
     with pytest.raises(ValueError):
         daso.DasoSync(daso.Schedule(**kw), torch.zeros(8), torch.zeros(8), [(0, 8)], 0.1, 0.9).fast_forward(
             E * nb + 1, losses)
+    with pytest.raises(ValueError, match="epoch losses"):     # 13 batches complete 2 epochs
+        daso.DasoSync(daso.Schedule(**kw), torch.zeros(8), torch.zeros(8), [(0, 8)], 0.1, 0.9).fast_forward(
+            13, losses[:1])
+    with pytest.raises(ValueError):
+        daso.DasoSync(daso.Schedule(**kw), torch.zeros(8), torch.zeros(8), [(0, 8)], 0.1, 0.9).fast_forward(
+            -1, losses)
