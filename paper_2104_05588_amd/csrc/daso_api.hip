@@ -117,6 +117,8 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     if (gr.ntiles > INT32_MAX) return DASO_EINVAL;
     max_tiles = std::max(max_tiles, gr.ntiles);
   }
+  // tile order across the XCDs, by the number of streams the launch touches
+  // (the measured rule is stated with the constants in daso_launch.h)
   int streams = 2;
   if (mode == daso::kModeAvg) streams = a.g + 1;
   if (mode == daso::kModeMerge) streams = a.P + 2 + (a.wire ? 1 : 0);
