@@ -52,6 +52,11 @@
  *    included), so empty buffers may be NULL.
  *  - On any error nothing is launched and a negative status is returned; the
  *    buffers are untouched.  daso_status_string names the status.
+ *  - Tile order: the fused step hands each XCD runs of consecutive tiles whose
+ *    length was measured best on MI355X (32768 elements below 20 streams).  The
+ *    environment variable DASO_FUSED_RUN_ELEMS (read once per process; 0 =
+ *    plain order) replaces that length, to reproduce the measurement.  The
+ *    order never changes a result.
  *  - Calls may be made from several host threads.  Fused steps with statistics
  *    share one small per-(device, stream) workspace (24 bytes per tile of 1024
  *    or 2048 parameters, plus a 260-byte table of bucket ranges) that the

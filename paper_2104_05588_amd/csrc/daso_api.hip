@@ -2,6 +2,7 @@
 // the per-stream statistics workspace, bucket grouping and launches.  Argument
 // checking is in daso_host.cpp.
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -94,6 +95,22 @@ void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr, int64_t tile
   a.ntiles = static_cast<int32_t>(std::max<int64_t>(t, 1));
 }
 
+// DASO_FUSED_RUN_ELEMS, when set to a non-negative number of elements, replaces
+// the measured run length of the fused step below kXcdRunMidStreams streams
+// (0: plain order).  The tile order never changes a result; the variable
+// exists to reproduce the measurements behind the default.  Read once.
+int64_t fused_run_elems() {
+  static const int64_t v = [] {
+    const char* e = getenv("DASO_FUSED_RUN_ELEMS");
+    if (e == nullptr || *e == '\0') return daso::kXcdRunFusedElems;
+    char* end = nullptr;
+    const long long x = strtoll(e, &end, 10);
+    return (end != e && *end == '\0' && x >= 0 && x <= (1LL << 30)) ? static_cast<int64_t>(x)
+                                                                    : daso::kXcdRunFusedElems;
+  }();
+  return v;
+}
+
 // The current device, which must also be the device of `stream` (kernels run
 // on the stream's device and the buffers and workspace live on the current one).
 int current_device(hipStream_t stream, int* dev) {
@@ -127,7 +144,7 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   if (streams >= daso::kXcdRunManyStreams) a.xcd_run = daso::kXcdRunMany;
   else if (streams >= daso::kXcdRunMidStreams) a.xcd_run = daso::kXcdRunMid;
   else if (mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams)
-    a.xcd_run = static_cast<int32_t>(std::max<int64_t>(1, daso::kXcdRunFusedElems / tile));
+    a.xcd_run = static_cast<int32_t>(std::max<int64_t>(1, fused_run_elems() / tile));
   std::unique_lock<std::mutex> hold;
   if (with_stats) {
     Workspace& w = workspace_entry(dev, stream);

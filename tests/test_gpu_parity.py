@@ -832,3 +832,50 @@ def test_fused_local_step_only(g):
     compare_fused(got, want, f"local step g={g}")
     got = run_fused(inp, bks, wire=False, stats=False)
     compare_fused(got, want, f"local step g={g} bare", wire=False, stats=False)
+
+
+_RUN_ORDER_SCRIPT = r"""
+import sys
+import numpy as np
+import torch
+sys.path.insert(0, sys.argv[1])
+import paper_2104_05588_amd as daso
+torch.cuda.set_device(0)
+n, g, P = 1_200_007, 4, 8
+bks = [(0, 500_003, 4), (500_003, n - 500_003, 2)]
+gen = torch.Generator(device="cuda")
+gen.manual_seed(77)
+x = torch.randn(n, generator=gen, device="cuda") * 0.02
+m = torch.randn(n, generator=gen, device="cuda") * 1e-3
+grads = [torch.randn(n, generator=gen, device="cuda") * 1e-3 for _ in range(g)]
+stale = [(x + torch.randn(n, generator=gen, device="cuda") * 1e-4).to(torch.bfloat16).view(torch.int16)
+         for _ in range(P)]
+wire = torch.empty(n, dtype=torch.int16, device="cuda")
+st = daso.new_stats(len(bks))
+daso.fused_sync_step(grads, x, m, stale, bks, 0.1, 0.9, 0.0, wire, None, st)
+torch.cuda.synchronize()
+out = np.concatenate([x.cpu().numpy().view(np.uint8), m.cpu().numpy().view(np.uint8),
+                      wire.cpu().numpy().view(np.uint8), st.cpu().numpy().ravel().view(np.uint8)])
+sys.stdout.buffer.write(out.tobytes())
+"""
+
+
+def test_tile_order_never_changes_a_result():
+    """DASO_FUSED_RUN_ELEMS changes only which XCD takes which tiles: plain
+    order, the default runs and longer or shorter runs give the same bits."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    outs = {}
+    for v in ("", "0", "4096", "65536", "1048576"):
+        announce("tile order, DASO_FUSED_RUN_ELEMS =", repr(v))
+        env = dict(os.environ, DASO_FUSED_RUN_ELEMS=v)
+        res = subprocess.run([sys.executable, "-c", _RUN_ORDER_SCRIPT, root], capture_output=True, env=env,
+                             timeout=110)
+        assert res.returncode == 0, res.stderr.decode()[-2000:]
+        outs[v] = res.stdout
+    base = outs[""]
+    assert len(base) > 0
+    for v, o in outs.items():
+        assert o == base, v
