@@ -27,7 +27,10 @@
  *     d = gbar + weight_decay * x[j]     (otherwise)
  *     m' = mu * m[j] + d ;  xl = x[j] - lr * m'
  *     P == 0:  x' = xl
- *     P >  0:  a = (2S) * xl ; a = a + widen(stale_i[j]) (i = 1..P) ; x' = a / (2S+P)
+ *     P >  0, S > 0:  a = (2S) * xl ; a = a + widen(stale_i[j]) (i = 1..P) ; x' = a / (2S+P)
+ *     P >  0, S = 0:  a = widen(stale_1[j]) ; a = a + widen(stale_i[j]) (i = 2..P) ; x' = a / P
+ *              (the blocking average of the copies: the local state is left out,
+ *              so a non-finite xl does not reach x')
  *     wire[j] = bf16_rne(x')   (or bf16_rne(xl) with DASO_PACK_PRE_MERGE)
  * widen(h) places the bf16 pattern h in the top half of a binary32 (exact); with
  * the fp32 exchange widen is the identity and the wire holds x' (or xl) itself.

@@ -24,8 +24,9 @@ order so that a GPU implementation can reproduce the same bits:
      model states that arrive S batches late:
          x' = (2S * xl + sum_{i=1..P} x_i) / (2S + P)
      computed as a = (2S) * xl ; a = a + x_i for i = 1..P ; x' = a / (2S + P);
-     with P = 0 the merge is the identity.  The x_i arrive as bf16 and are
-     widened exactly (bits << 16).
+     with P = 0 the merge is the identity.  S = 0 (blocking synchronisation)
+     is the plain average: a = x_1 ; a = a + x_i for i = 2..P ; x' = a / P.
+     The x_i arrive as bf16 and are widened exactly (bits << 16).
   4. buffer packaging for the exchange (Section 3: the send buffer holds a
      16-bit rendering of the parameters, widened again by the receiver;
      Section 4: DASO uses bfloat16): wire = bf16_rne(x').
@@ -122,15 +123,26 @@ def _received(st: np.ndarray) -> np.ndarray:
 def merge_eq1(xl: np.ndarray, stale: Sequence[np.ndarray], S: int) -> np.ndarray:
     """Eq. (1): staleness-weighted average of the local state xl with the P
     exchanged states (bf16 bit patterns or fp32), local weight 2S, each copy
-    weight 1."""
+    weight 1.
+
+    S = 0 is the blocking global synchronisation of the warm-up and cool-down
+    phases (Section 3): the result is the plain average of the P exchanged
+    states (this GPU's own state is one of them), so the local term is left
+    out rather than multiplied by zero, and a non-finite local state does not
+    reach the result."""
     if S < 0:
         raise ValueError("S must be >= 0")
     P = len(stale)
     xl = np.asarray(xl, dtype=np.float32)
     if P == 0:
         return xl.copy()
-    a = F32(2 * S) * xl
-    for st in stale:
+    if S == 0:
+        a = np.array(_received(stale[0]), dtype=np.float32, copy=True)
+        rest = stale[1:]
+    else:
+        a = F32(2 * S) * xl
+        rest = stale
+    for st in rest:
         a = a + _received(st)
     return a / F32(2 * S + P)
 

@@ -228,6 +228,15 @@ __device__ __forceinline__ void store_avg(const StepArgs& a, int64_t e0, unsigne
   else if (a.gavg) store_f32<FULL, false>(a.gavg, e0, mask, gbar);
 }
 
+// The start of Eq. (1)'s sum: the local term 2S * xl.  S = 0 is the blocking
+// synchronisation of Section 3, the plain average of the exchanged copies, so
+// the local state is left out: the sum starts from -0, the identity of IEEE
+// addition (-0 + c == c for every c), and a non-finite xl cannot reach it.
+__device__ __forceinline__ f32x4 merge_start(float two_s, f32x4 xl) {
+  if (two_s != 0.0f) return two_s * xl;
+  return f32x4{-0.0f, -0.0f, -0.0f, -0.0f};
+}
+
 // The optimizer step (Section 3.1; PyTorch SGD with momentum, coupled weight
 // decay that is skipped when zero): the local state xl; m becomes the new
 // momentum.
@@ -284,7 +293,7 @@ __device__ __forceinline__ void step_vec(const StepArgs& a, int64_t e0, unsigned
 
   f32x4 xn = xl;
   if (P > 0) {
-    f32x4 acc4 = two_s * xl;
+    f32x4 acc4 = merge_start(two_s, xl);
 #pragma unroll
     for (int i = 0; i < P; ++i) acc4 = acc4 + received<XF>(load_x<XF, FULL>(a.stale[i], e0, mask));
     xn = divide(acc4, qm);
@@ -357,7 +366,7 @@ __device__ __forceinline__ void finish(const StepArgs& a, int64_t e0, unsigned m
   f32x4 xn = xl;
   if constexpr (V::kP > 0) {
     if (PP >= 0 || a.P > 0) {
-      f32x4 acc4 = two_s * xl;
+      f32x4 acc4 = merge_start(two_s, xl);
 #pragma unroll
       for (int i = 0; i < V::kP; ++i)
         if (PP >= 0 || i < a.P) acc4 = acc4 + received<XF>(v.s[i]);

@@ -396,6 +396,46 @@ def test_fused_special_values(seed):
         assert sum(s[2] for s in got["stats"]) > 0
 
 
+@pytest.mark.parametrize("g,P,f32", [(4, 8, False), (3, 5, False), (9, 40, False), (8, 32, False),
+                                     (4, 8, True), (5, 7, True)])
+def test_zero_staleness_ignores_a_nonfinite_local_state(g, P, f32):
+    """S = 0 (blocking average): a NaN or infinite local state leaves the merged
+    value the plain mean of the finite copies; copies that are all -0 give -0.
+    Buckets with S = 0 sit next to buckets with S > 0 (whose results do take
+    the non-finite local state).  Fused step and the merge entry points, with
+    exact, bounded and run-time stream counts, bf16 and fp32 exchange."""
+    rng = np.random.default_rng(1000 + 10 * g + P + (5 if f32 else 0))
+    n = 9_001
+    inp = random_inputs(rng, n, g, P)
+    for pos in (rng.integers(0, n, 300), rng.integers(0, n, 300), rng.integers(0, n, 300)):
+        inp["params"][pos] = rng.choice(np.array([np.nan, np.inf, -np.inf], F32), pos.size)
+    negz = rng.integers(0, n, 40)
+    for st in inp["stale"]:
+        st[negz] = 0x8000
+    if f32:
+        inp["stale"] = [O.bf16_widen(s) for s in inp["stale"]]
+    bks = [(0, 3000, 0), (3000, 1001, 2), (4001, 5000, 0)]
+    announce("S=0 non-finite local state g=", g, "P=", P, "f32=", f32)
+    exch = "f32" if f32 else "bf16"
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
+                             0.1, 0.9, 0.0, exchange=exch)
+    zero_s = np.r_[0:3000, 4001:9001]
+    assert np.all(np.isfinite(want["params"][zero_s]))
+    assert not np.all(np.isfinite(want["x_local"][zero_s]))
+    assert np.all(want["params"].view(np.uint32)[negz[negz < 3000]] == 0x80000000)
+    got = run_fused(inp, bks, f32=f32)
+    compare_fused(got, want, f"S=0 fused g={g} P={P} f32={f32}")
+    # the merge entry point on the same local state
+    xl = want["x_local"]
+    mwant, mwire = O.global_merge(xl, inp["stale"], bks, pack=True, exchange=exch)
+    xd = dev_f32(xl)
+    wd_ = torch.empty(n, dtype=torch.float32 if f32 else torch.int16, device="cuda")
+    daso.global_merge(xd, [(dev_f32 if f32 else dev_bf16)(a) for a in inp["stale"]], bks, wd_)
+    torch.cuda.synchronize()
+    check_f32(host_f32(xd), mwant, f"S=0 merge P={P} f32={f32}")
+    (check_f32 if f32 else check_u16)(host_f32(wd_) if f32 else host_u16(wd_), mwire, f"S=0 merge wire P={P}")
+
+
 def test_fused_without_optional_outputs():
     rng = np.random.default_rng(31)
     n = 33_333

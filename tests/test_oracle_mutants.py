@@ -101,8 +101,51 @@ def _stats_abs_not_square(gbar, xl, x_new):
 
 
 _true_bucket_stats = O.bucket_stats
+_true_global_merge = O.global_merge
+_true_fused_sync_step = O.fused_sync_step
+
+
+def _one_S_for_every_bucket(buckets):
+    return [(s, k, buckets[0][2]) for (s, k, _) in buckets]
+
+
+def _neighbour_bucket_S(buckets):
+    nb = len(buckets)
+    return [(s, k, buckets[(b + 1) % nb][2]) for b, (s, k, _) in enumerate(buckets)]
+
+
+def _global_merge_one_S(params, stale, buckets, *a, **k):
+    return _true_global_merge(params, stale, _one_S_for_every_bucket(buckets), *a, **k)
+
+
+def _global_merge_neighbour_S(params, stale, buckets, *a, **k):
+    return _true_global_merge(params, stale, _neighbour_bucket_S(buckets), *a, **k)
+
+
+def _fused_one_S(grads, params, momentum, stale, buckets, *a, **k):
+    return _true_fused_sync_step(grads, params, momentum, stale, _one_S_for_every_bucket(buckets), *a, **k)
+
+
+def _fused_neighbour_S(grads, params, momentum, stale, buckets, *a, **k):
+    return _true_fused_sync_step(grads, params, momentum, stale, _neighbour_bucket_S(buckets), *a, **k)
+
+
+def _merge_zero_S_keeps_local_term(xl, stale, S):
+    P = len(stale)
+    if P == 0:
+        return np.array(xl, dtype=np.float32, copy=True)
+    a = F32(2 * S) * np.asarray(xl, dtype=np.float32)
+    for st in stale:
+        a = a + O.bf16_widen(st)
+    return a / F32(2 * S + P)
+
 
 MUTANTS = [
+    ("global_merge", _global_merge_one_S, [pins.test_per_bucket_staleness_matches_exact_rational_eq1]),
+    ("global_merge", _global_merge_neighbour_S, [pins.test_per_bucket_staleness_matches_exact_rational_eq1]),
+    ("fused_sync_step", _fused_one_S, [pins.test_per_bucket_staleness_matches_exact_rational_eq1]),
+    ("fused_sync_step", _fused_neighbour_S, [pins.test_per_bucket_staleness_matches_exact_rational_eq1]),
+    ("merge_eq1", _merge_zero_S_keeps_local_term, [pins.test_merge_zero_staleness_ignores_the_local_state]),
     ("merge_eq1", _merge_S_not_2S, [pins.test_merge_gradient_form_appendix,
                                     pins.test_merge_small_integers_match_exact_rational_eq1]),
     ("merge_eq1", _merge_wrong_denominator, [pins.test_merge_weights_sum_to_one,

@@ -273,6 +273,67 @@ def test_merge_zero_staleness_is_plain_mean_of_copies():
         assert np.max(np.abs(got - want) / np.maximum(np.abs(want), 1e-30)) <= (P + 1) * 2.0 ** -24 * 8
 
 
+def test_merge_zero_staleness_ignores_the_local_state():
+    """S = 0 is the blocking average of the exchanged states (Section 3, warm-up
+    and cool-down phases): the local state has weight zero and does not enter,
+    so a NaN or infinite local state still gives the exact mean of finite
+    copies, and copies that are all -0 average to -0 (an IEEE sum of -0s)."""
+    rng = np.random.default_rng(120)
+    n = 64
+    xl = rng.standard_normal(n).astype(F32)
+    xl[0::3] = np.nan
+    xl[1::3] = np.inf
+    xl[2::6] = -np.inf
+    for P in (1, 2, 3, 5):
+        ints = [rng.integers(-200, 200, n) for _ in range(P)]
+        st = [O.bf16_rne(v.astype(F32)) for v in ints]
+        got = O.merge_eq1(xl, st, 0)
+        for j in range(n):
+            want = frac_to_f32(Fraction(sum(int(v[j]) for v in ints), P))
+            assert f32_bits(got[j:j + 1])[0] == f32_bits(np.array([want], F32))[0], (P, j)
+    negz = [np.full(n, 0x8000, np.uint16) for _ in range(3)]
+    got = O.merge_eq1(xl, negz, 0)
+    assert np.all(f32_bits(got) == 0x80000000)
+
+
+def _per_bucket_case():
+    """Small exact case: integers for params, gradients and copies, lr = mu = 1/2
+    and a zero momentum buffer, so gbar (half-integers), the local state
+    xl = x - gbar/2 (quarter-integers) and every partial sum of Eq. (1) are exact
+    binary32 values and only the final division rounds.  The buckets are given
+    out of order, with S = 3, 1, 8, 0 and an empty bucket with S = 5."""
+    rng = np.random.default_rng(121)
+    n, P = 40, 5
+    x_i = rng.integers(-64, 65, n)
+    g_i = [rng.integers(-64, 65, n) for _ in range(2)]
+    c_i = [rng.integers(-200, 201, n) for _ in range(P)]
+    buckets = [(24, 9, 3), (0, 10, 1), (10, 0, 5), (33, 7, 8), (10, 14, 0)]
+    S_of = np.empty(n, np.int64)
+    for (s, k, S) in buckets:
+        S_of[s:s + k] = S
+    xl = [Fraction(int(x_i[j])) - Fraction(int(g_i[0][j]) + int(g_i[1][j]), 4) for j in range(n)]
+    want = []
+    for j in range(n):
+        S = int(S_of[j])
+        num = 2 * S * xl[j] + sum(Fraction(int(c[j])) for c in c_i)
+        want.append(frac_to_f32(num / (2 * S + P)))
+    return {"x": x_i.astype(F32), "grads": [g.astype(F32) for g in g_i],
+            "stale": [O.bf16_rne(c.astype(F32)) for c in c_i], "buckets": buckets,
+            "xl": np.array([float(v) for v in xl], F32), "want": np.array(want, F32)}
+
+
+def test_per_bucket_staleness_matches_exact_rational_eq1():
+    """Each element is merged with the S of its own bucket, whatever the order in
+    which the buckets are listed: global_merge and fused_sync_step against Eq. (1)
+    evaluated exactly, element by element, with that element's bucket's S."""
+    c = _per_bucket_case()
+    got, wire = O.global_merge(c["xl"], c["stale"], c["buckets"], pack=True)
+    assert np.array_equal(f32_bits(got), f32_bits(c["want"]))
+    out = O.fused_sync_step(c["grads"], c["x"], np.zeros_like(c["x"]), c["stale"], c["buckets"], 0.5, 0.5, 0.0)
+    assert np.array_equal(f32_bits(out["x_local"]), f32_bits(c["xl"]))
+    assert np.array_equal(f32_bits(out["params"]), f32_bits(c["want"]))
+
+
 def test_merge_gradient_form_appendix():
     """Appendix, gradient form of the global synchronisation:
     x_DASO = x_t - alpha (2S sum_{k<S} G_l,k + sum_i G_p,i), alpha = eta/(2S+P),
