@@ -53,8 +53,13 @@
  *  - n == 0 is a valid no-op: once the counts and flags are checked the call
  *    returns DASO_OK without looking at any pointer or buffer (statistics
  *    included), so empty buffers may be NULL.
- *  - On any error nothing is launched and a negative status is returned; the
- *    buffers are untouched.  daso_status_string names the status.
+ *  - On an argument error (DASO_EINVAL, DASO_EALIGN, DASO_EALIAS) nothing is
+ *    launched and the buffers are untouched; daso_status_string names the
+ *    status.  A call may queue more than one kernel: one per 64 buckets of its
+ *    table, and a statistics pass after each fused launch with statistics.  If
+ *    queueing one of them fails (DASO_EHIP), the kernels queued before it still
+ *    run: the outputs (params, momentum, wire, grad_avg, stats) of the buckets
+ *    they cover may then already be updated, the others are untouched.
  *  - Tile order: the fused step hands each XCD runs of consecutive tiles whose
  *    length was measured best on MI355X (32768 elements below 20 streams).  The
  *    environment variable DASO_FUSED_RUN_ELEMS (read once per process; 0 =

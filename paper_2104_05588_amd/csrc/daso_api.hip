@@ -158,7 +158,9 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   for (const auto& gr : groups) {
     fill_group(a, b, gr, tile);
     a.stats = with_stats ? stats + gr.first : nullptr;
-    if (daso::launch_step(mode, with_stats, a, stream) != hipSuccess) return DASO_EHIP;
+    const int64_t grid = daso::host::launch_grid(a.ntiles, a.xcd_run);
+    if (daso::launch_step(mode, with_stats, a, static_cast<uint32_t>(grid), stream) != hipSuccess)
+      return DASO_EHIP;
   }
   return DASO_OK;
 }

@@ -149,6 +149,14 @@ int check_fused(const daso_sync_args& s, FusedView* view) {
   return DASO_OK;
 }
 
+int64_t launch_grid(int64_t ntiles, int32_t run) {
+  if (ntiles < 1) return 1;
+  if (ntiles <= kMaxGrid) return ntiles;
+  const int64_t block = 8 * static_cast<int64_t>(run < 1 ? 1 : run);
+  const int64_t whole = (kMaxGrid / block) * block;
+  return whole > 0 ? whole : kMaxGrid;
+}
+
 }  // namespace host
 }  // namespace daso
 

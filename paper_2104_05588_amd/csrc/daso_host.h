@@ -24,6 +24,15 @@ struct FusedView {
   bool xf32;
 };
 
+// Workgroups of a launch over `ntiles` tiles (one 256-thread workgroup per
+// tile) whose XCD runs are `run` tiles long: one per tile up to kMaxGrid, the
+// largest multiple of the run block (8 * run) within kMaxGrid beyond that, the
+// kernel looping over the remaining tiles.  The dispatch packet counts the grid
+// in work-items in 32 bits, so a grid of 256-thread workgroups must stay below
+// 2^24; kMaxGrid (4096 workgroups per CU) is far above what fills the chip.
+constexpr int64_t kMaxGrid = int64_t(1) << 20;
+int64_t launch_grid(int64_t ntiles, int32_t run);
+
 // Each returns DASO_OK or the status the entry point must return; n == 0 is
 // DASO_OK once the counts are valid (the caller then launches nothing).
 int check_local_avg(const float* const* grads, int32_t g, const float* out, int64_t n);

@@ -465,7 +465,8 @@ __device__ __forceinline__ int xcd_runs(int w, int grid, int run) {
   return (j / run) * block + x * run + (j % run);
 }
 
-// One workgroup per tile; the loop also serves a grid smaller than the tiles.
+// One workgroup per tile; the loop serves a grid smaller than the tiles (the
+// host caps the grid for launches of more than 2^20 tiles).
 template <int MODE, int G, int PP, bool STATS, bool XF>
 __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   constexpr int64_t kTile = tile_of<MODE, G, PP, XF>();
@@ -658,12 +659,13 @@ auto dispatch(Mode mode, bool with_stats, const StepArgs& a, const F& f) {
 // this call nor consumed by it.
 struct Launcher {
   const StepArgs& a;
+  uint32_t grid;
   hipStream_t stream;
   template <int MODE, int G, int PP, bool STATS, bool XF>
   hipError_t run() const {
     void* args[] = {const_cast<StepArgs*>(&a)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&step_kernel<MODE, G, PP, STATS, XF>),
-                                         dim3(a.ntiles), dim3(kBlock), args, 0, stream);
+                                         dim3(grid), dim3(kBlock), args, 0, stream);
     if (e != hipSuccess || !STATS) return e;
     StatsArgs sa = {a.partials, a.tile_table, a.stats, a.nb};
     void* sargs[] = {&sa};
@@ -684,8 +686,8 @@ int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& a) {
   return dispatch(mode, with_stats, a, TileSize{});
 }
 
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, hipStream_t stream) {
-  return dispatch(mode, with_stats, a, Launcher{a, stream});
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, uint32_t grid, hipStream_t stream) {
+  return dispatch(mode, with_stats, a, Launcher{a, grid, stream});
 }
 
 }  // namespace daso

@@ -111,8 +111,9 @@ inline int64_t tiles_of(int64_t start, int64_t end, int64_t tile) {
 // arguments (mode, stream counts, exchange type).
 int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& args);
 
-// Enqueue one launch of `mode` over the buckets in `args`, one workgroup per
-// tile (args.ntiles, counted with tile_elems()).
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, hipStream_t stream);
+// Enqueue one launch of `mode` over the buckets in `args` (args.ntiles tiles,
+// counted with tile_elems()) on `grid` workgroups: one per tile, or fewer, each
+// then looping over tiles grid apart.
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, uint32_t grid, hipStream_t stream);
 
 }  // namespace daso

@@ -203,12 +203,33 @@ static void schedule_checks(std::mt19937_64& rng) {
   daso_schedule_destroy(nullptr);
 }
 
+// The launch grid: one workgroup per tile up to the cap, a whole number of
+// XCD-run blocks beyond it, and always within the 32-bit work-item count of a
+// dispatch of 256-thread workgroups.
+static void grid_checks() {
+  const int64_t cap = daso::host::kMaxGrid;
+  EXPECT(cap * 256 < (int64_t(1) << 32));
+  const int32_t runs[] = {1, 2, 3, 16, 32, 40, 1 << 20};
+  const int64_t counts[] = {1, 2, 255, 256, 4097, cap - 1, cap, cap + 1, 3 * cap + 7,
+                            int64_t(1) << 24, (int64_t(1) << 31) - 1};
+  for (int32_t run : runs) {
+    for (int64_t nt : counts) {
+      const int64_t g = daso::host::launch_grid(nt, run);
+      EXPECT(g >= 1 && g <= cap && g <= nt);
+      if (nt <= cap) EXPECT(g == nt);
+      if (nt > cap && 8 * int64_t(run) <= cap) EXPECT(g % (8 * int64_t(run)) == 0 && g > cap - 8 * int64_t(run));
+    }
+  }
+  EXPECT(daso::host::launch_grid(0, 1) == 1);
+}
+
 int main() {
   std::mt19937_64 rng(2104);
   bucket_checks(rng);
   planner_checks(rng);
   argument_checks();
   schedule_checks(rng);
+  grid_checks();
   if (failures) std::fprintf(stderr, "%d expectation(s) failed\n", failures);
   else std::printf("host checks ok\n");
   return failures ? 1 : 0;
