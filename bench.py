@@ -23,8 +23,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD published peak
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "fused_sync_resnet50_counters.txt")
+# sources whose change invalidates the committed counter figures: the kernels,
+# their launch interface and the host code that picks the tile order and grid
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2104_05588_amd", "csrc", f)
-                  for f in ("daso_kernels.hip", "daso_launch.h")]
+                  for f in ("daso_kernels.hip", "daso_launch.h", "daso_api.hip")]
+PROBE_LIB = os.path.join(ROOT, "paper_2104_05588_amd", "libdaso_ceiling.so")
 
 
 def kernel_source_sha() -> str:
@@ -51,6 +54,143 @@ def counter_traffic(workload: str):
         return float(kv["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+# ------------------------------------------------------- bandwidth ceilings
+class Probes:
+    """The access-pattern probes of libdaso_ceiling.so (built by build()): the
+    fused step's loads and stores on its own buffers, tile grid and tile order,
+    without its arithmetic; and a one-stream copy."""
+
+    def __init__(self, torch):
+        import ctypes
+        if not os.path.exists(PROBE_LIB):
+            raise RuntimeError(f"{PROBE_LIB} is missing: build it with `python -m paper_2104_05588_amd.build`")
+        self.torch, self.ct = torch, ctypes
+        self.lib = ctypes.CDLL(PROBE_LIB)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        self.lib.daso_probe_run.argtypes = [ctypes.POINTER(vp), i32, ctypes.POINTER(vp), i32, ctypes.POINTER(vp),
+                                            i32, ctypes.POINTER(vp), i32, vp, i64, i32, i32, vp]
+        self.lib.daso_probe_run.restype = ctypes.c_int
+        self.sink = torch.zeros(4, dtype=torch.int32, device="cuda")
+
+    def _arr(self, ts, n, esz):
+        arr = (self.ct.c_void_p * max(len(ts), 1))()
+        for i, t in enumerate(ts):
+            if not t.is_cuda or not t.is_contiguous() or t.element_size() != esz or t.numel() < n:
+                raise ValueError("probe streams must be contiguous device buffers of at least n elements")
+            arr[i] = t.data_ptr()
+        return arr
+
+    def call(self, rd32, rd16, wr32, wr16, n, iters, xcd_run):
+        """A callable that launches the probe once on the current stream."""
+        args = (self._arr(rd32, n, 4), len(rd32), self._arr(rd16, n, 2), len(rd16), self._arr(wr32, n, 4),
+                len(wr32), self._arr(wr16, n, 2), len(wr16), self.ct.c_void_p(self.sink.data_ptr()),
+                self.ct.c_int64(n), iters, xcd_run)
+        keep = (rd32, rd16, wr32, wr16)
+        torch = self.torch
+
+        def run():
+            _ = keep
+            rc = self.lib.daso_probe_run(*args, self.ct.c_void_p(torch.cuda.current_stream().cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"daso_probe_run failed with {rc}")
+        return run
+
+
+def step_tile_and_run(g: int, P: int, wire: bool = True):
+    """Tile size and XCD run length the library takes for a fused step with bf16
+    copies and g, P at a node shape (the rule stated in daso_launch.h): tiles of
+    2048 elements when a vector's inputs take at most 48 registers (4g + 2P + 8),
+    else 1024; runs of 32 tiles from 32 streams, 16 from 20, 32K elements from 9."""
+    tile = 2048 if 4 * g + 2 * P + 8 <= 48 else 1024
+    streams = g + P + 4 + (1 if wire else 0)
+    if streams >= 32:
+        return tile, 32
+    if streams >= 20:
+        return tile, 16
+    if streams >= 9:
+        return tile, max(1, 32768 // tile)
+    return tile, 1
+
+
+def time_cold(torch, fn, reps, scratch):
+    """Median and minimum of `reps` calls, each after a 1 GiB write that evicts
+    the 256 MB Infinity Cache, with HIP events around the call on its stream."""
+    stream = torch.cuda.current_stream()
+    ts = []
+    for i in range(reps):
+        scratch.fill_(float(i))
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        b.synchronize()
+        ts.append(a.elapsed_time(b) * 1e3)
+    ts.sort()
+    return ts[len(ts) // 2], ts[0]
+
+
+def time_warm(torch, fn, reps):
+    """Average over `reps` calls back to back between one pair of HIP events."""
+    stream = torch.cuda.current_stream()
+    fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        fn()
+    b.record(stream)
+    b.synchronize()
+    return a.elapsed_time(b) * 1e3 / reps
+
+
+def copy_rate(torch, probes, reps=10):
+    """A 1 GiB device copy by the probe library's copy kernel (16 bytes per lane,
+    plain tile order), back to back: read plus written bytes per second."""
+    n = 1 << 28
+    src = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    us = time_warm(torch, probes.call([src], [], [dst], [], n, 2, 1), reps)
+    del src, dst
+    return 2 * 4 * n / (us * 1e-6) / 1e9
+
+
+def ceiling(torch, probes, w, inp, wire, step, reps):
+    """The step and its access pattern on the step's own buffers, tile grid and
+    tile order, each cold (cache evicted before every call) and warm (back to
+    back): the reads alone (g + 2 fp32 and P bf16 streams), the writes alone
+    (params and momentum fp32, the wire bf16), both mixed as a bare kernel, and
+    the separated bound = reads alone + writes alone."""
+    n = w.n
+    tile, run = step_tile_and_run(w.g, w.P)
+    it = tile // 1024
+    rd32 = list(inp["grads"]) + [inp["params"], inp["momentum"]]
+    rd16 = list(inp["stale"])
+    wr32, wr16 = [inp["params"], inp["momentum"]], [wire]
+    read_b = n * (4 * len(rd32) + 2 * len(rd16))
+    write_b = n * 10
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    fns = {"step": step,
+           "reads_alone": probes.call(rd32, rd16, [], [], n, it, run),
+           "writes_alone": probes.call([], [], wr32, wr16, n, it, run),
+           "bare_mix": probes.call(rd32, rd16, wr32, wr16, n, it, run)}
+    out = {"tile_elems": tile, "xcd_run_tiles": run, "read_bytes": read_b, "write_bytes": write_b}
+    for name, fn in fns.items():
+        med, mn = time_cold(torch, fn, reps, scratch)
+        out[name] = {"cold_median_us": med, "cold_min_us": mn, "warm_us": time_warm(torch, fn, reps)}
+    del scratch
+    for name, b in (("reads_alone", read_b), ("writes_alone", write_b), ("bare_mix", read_b + write_b),
+                    ("step", read_b + write_b)):
+        out[name]["cold_GBps"] = b / (out[name]["cold_median_us"] * 1e-6) / 1e9
+    sep = out["reads_alone"]["cold_median_us"] + out["writes_alone"]["cold_median_us"]
+    sep_warm = out["reads_alone"]["warm_us"] + out["writes_alone"]["warm_us"]
+    out["separated_bound_cold_us"] = sep
+    out["separated_bound_cold_frac"] = (read_b + write_b) / (sep * 1e-6) / 1e9 / PEAK_HBM_GBPS
+    out["step_cold_over_separated"] = sep / out["step"]["cold_median_us"]
+    out["separated_bound_warm_us"] = sep_warm
+    out["step_warm_over_separated"] = sep_warm / out["step"]["warm_us"]
+    return out
 
 
 def cpu_baseline(w, budget_s: float):
@@ -102,7 +242,10 @@ def main() -> int:
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
-                    help="run only a plain device copy of known size (counter calibration)")
+                    help="run only a plain 1 GiB device copy, --steps times (counter calibration)")
+    ap.add_argument("--ceiling", action="store_true",
+                    help="time only the step and its access-pattern probes (reads alone, writes alone, bare "
+                         "mix; --steps calls each, cold and warm) and a 1 GiB copy; prints one JSON line")
     ap.add_argument("--node-shapes", action="store_true",
                     help="time every node shape (g = 4 or 8 replicas, P = 0 to 32 copies, bf16 and fp32 "
                          "exchange) on the resnet50-shaped parameter set instead of the one workload")
@@ -125,14 +268,17 @@ def main() -> int:
     torch.cuda.set_device(0)
     daso.load()
 
+    probes = Probes(torch)
     if args.copy_probe:
         nbytes = 1 << 30
         src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)
+        copy = probes.call([src], [], [dst], [], nbytes // 4, 2, 1)
         for _ in range(args.steps):
-            dst.copy_(src)
+            copy()
         torch.cuda.synchronize()
-        print(json.dumps({"copy_probe_bytes": nbytes, "dispatches": args.steps}), flush=True)
+        print(json.dumps({"copy_probe_bytes": nbytes, "dispatches": args.steps,
+                          "kernel": "probe_kernel<1,0,1,0,2> (16-byte lanes)"}), flush=True)
         return 0
 
     if args.node_shapes:
@@ -151,6 +297,13 @@ def main() -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+
+    if args.ceiling:
+        ceil = ceiling(torch, probes, w, inp, wire, step, max(5, min(args.steps, 50)))
+        print(json.dumps({"workload": f"{w.name}-shaped parameter set", "params": n, "g": w.g, "P": w.P,
+                          "ceiling": ceil, "device_copy_GBps": copy_rate(torch, probes),
+                          "peak_GBps": PEAK_HBM_GBPS}), flush=True)
+        return 0
 
     # the timed region: K calls back to back on the stream the kernels run on,
     # bracketed by one pair of HIP events (events between the calls would add
@@ -193,18 +346,8 @@ def main() -> int:
     cold.sort()
     del scratch
 
-    # plain device copy of the same footprint class, for context
-    cp_src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
-    cp_dst = torch.empty_like(cp_src)
-    cp_dst.copy_(cp_src)
-    cs, ce = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    cs.record(stream)
-    for _ in range(10):
-        cp_dst.copy_(cp_src)
-    ce.record(stream)
-    torch.cuda.synchronize()
-    copy_gbps = 10 * 2 * cp_src.numel() * 4 / (cs.elapsed_time(ce) * 1e-3) / 1e9
-    del cp_src, cp_dst
+    # a plain 1 GiB device copy (the probe library's 16-byte-lane copy kernel), for context
+    copy_gbps = copy_rate(torch, probes)
 
     # the separate entry points on the same workload, for context, timed as the
     # step is: calls back to back between one pair of events, so that the host's
@@ -288,6 +431,11 @@ def main() -> int:
         graph_replay = {"error": str(e)}
     achieved = alg_bytes / (avg_ms * 1e-3) / 1e9
     traffic = counter_traffic(w.name)
+    cold_frac = alg_bytes / (cold[len(cold) // 2] * 1e-3) / 1e9 / PEAK_HBM_GBPS
+    # last, since the probes overwrite params and momentum: the step's access
+    # pattern on its own buffers without its arithmetic (reads alone, writes
+    # alone, both mixed), cold and warm
+    ceil = ceiling(torch, probes, w, inp, wire, step, max(5, min(args.steps, 20)))
 
     out = {
         "metric": "params synced/sec and achieved HBM GB/s (% of peak) per fused DASO sync step",
@@ -313,8 +461,11 @@ def main() -> int:
                      "kernel_avg_us": avg_ms * 1e3, "per_call_median_us": med_ms * 1e3,
                      "per_call_min_us": per_call[0] * 1e3,
                      "kernel_cold_median_us": cold[len(cold) // 2] * 1e3,
-                     "cold_frac": alg_bytes / (cold[len(cold) // 2] * 1e-3) / 1e9 / PEAK_HBM_GBPS,
-                     "device_copy_GBps": copy_gbps},
+                     "cold_frac": cold_frac,
+                     # the resnet50-shaped target (80% of peak) is stated for the cold figure
+                     "target": {"figure": "cold_frac", "frac": 0.80, "met": cold_frac >= 0.80},
+                     "device_copy_GBps": copy_gbps,
+                     "ceiling": ceil},
         "entry_points": entry_points,
         "graph_replay": graph_replay,
     }

@@ -20,6 +20,10 @@ CAPI_CLUSTER_SRC = os.path.join(ROOT, "tests", "c", "daso_cluster_capi.c")
 CAPI_CLUSTER = os.path.join(PKG, "daso_cluster_capi")
 
 SOURCES = ["daso_kernels.hip", "daso_api.hip", "daso_host.cpp", "daso_schedule.cpp"]
+# The bench's bandwidth-ceiling probes (the step's access pattern without its
+# arithmetic): a library of their own, outside the C ABI.
+PROBE_SOURCE = "daso_ceiling.hip"
+PROBE_LIB = os.path.join(PKG, "libdaso_ceiling.so")
 
 # Numerics flags: binary32 operations must be evaluated exactly as written (no
 # contraction into FMA, correctly rounded division, subnormals kept), so the
@@ -56,9 +60,24 @@ def build(verbose: bool = False) -> str:
     if verbose and errs:
         sys.stderr.write("\n".join(errs) + "\n")
     os.replace(tmp, LIB)
+    build_probes(verbose)
     if os.path.exists(CAPI_CLIENT_SRC):
         build_capi_client(verbose)
     return LIB
+
+
+def build_probes(verbose: bool = False) -> str:
+    """libdaso_ceiling.so: the access-pattern probes that bench.py times."""
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc(), *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, os.path.join(CSRC, PROBE_SOURCE), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"hipcc failed with status {res.returncode}")
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 def build_capi_client(verbose: bool = False) -> str:

@@ -1,0 +1,162 @@
+// Bandwidth ceilings of the fused step's memory access pattern, for the bench
+// only (a library of its own, outside the C ABI of include/daso.h).
+//
+// Each probe kernel makes exactly the loads and stores of a fused step, on the
+// same tile grid, tile size and tile order, with the same access widths (16
+// bytes per lane for fp32 streams, 8 for bf16) and non-temporal hints, and none
+// of its arithmetic: R32 fp32 and R16 bf16 streams read, W32 fp32 and W16 bf16
+// streams written.  Taking the reads alone, the writes alone and both mixed,
+// they measure what the step's access mix can reach on a given part; a one-
+// stream copy gives the plain copy rate.
+//
+// Safety: every stream holds at least n elements and n is a multiple of 4
+// (checked by daso_probe_run before any launch), so a thread touches the
+// 4-element vector at element e0 only when e0 < n, which keeps the whole vector
+// inside every buffer.  The grid is at most the tile count, each workgroup
+// looping over tiles grid apart, so every tile is visited once.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "daso_launch.h"
+
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kProbeBlock = 256;
+constexpr int kMaxRead = 48;
+constexpr int kMaxWrite = 4;
+
+struct ProbeArgs {
+  const void* rd32[kMaxRead];  // fp32 streams read
+  const void* rd16[kMaxRead];  // bf16 streams read
+  void* wr32[kMaxWrite];       // fp32 streams written
+  void* wr16[kMaxWrite];       // bf16 streams written
+  uint32_t* sink;              // one word: a read-only probe stores its fold here when sink_flag != 0
+  int64_t n;                   // elements per stream, a multiple of 4
+  int32_t ntiles;
+  int32_t xcd_run;
+  int32_t sink_flag;           // 0 in every run; keeps the loads of a read-only probe alive
+};
+
+template <int R32, int R16, int W32, int W16, int ITERS>
+__global__ __launch_bounds__(kProbeBlock) void probe_kernel(const ProbeArgs a) {
+  constexpr int64_t kTile = int64_t(kProbeBlock) * 4 * ITERS;
+  const int w0 = a.xcd_run > 1 ? daso::xcd_runs(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), a.xcd_run)
+                               : static_cast<int>(blockIdx.x);
+  for (int64_t t = w0; t < a.ntiles; t += gridDim.x) {
+    const int64_t base = t * kTile + int64_t(threadIdx.x) * 4;
+    u32x4 r32[ITERS][R32 > 0 ? R32 : 1];
+    u32x2 r16[ITERS][R16 > 0 ? R16 : 1];
+    // every load of the thread's vectors first, as the step issues them
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int64_t e0 = base + int64_t(it) * kProbeBlock * 4;
+      if (e0 < a.n) {
+#pragma unroll
+        for (int s = 0; s < R32; ++s)
+          r32[it][s] = __builtin_nontemporal_load(static_cast<const u32x4*>(a.rd32[s]) + e0 / 4);
+#pragma unroll
+        for (int s = 0; s < R16; ++s)
+          r16[it][s] = __builtin_nontemporal_load(static_cast<const u32x2*>(a.rd16[s]) + e0 / 4);
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+      const int64_t e0 = base + int64_t(it) * kProbeBlock * 4;
+      if (e0 >= a.n) continue;
+      u32x4 v = {static_cast<uint32_t>(e0), 1u, 2u, 3u};
+#pragma unroll
+      for (int s = 0; s < R32; ++s) v ^= r32[it][s];
+#pragma unroll
+      for (int s = 0; s < R16; ++s) {
+        v.x ^= r16[it][s].x;
+        v.y ^= r16[it][s].y;
+      }
+#pragma unroll
+      for (int w = 0; w < W32; ++w) __builtin_nontemporal_store(v, static_cast<u32x4*>(a.wr32[w]) + e0 / 4);
+#pragma unroll
+      for (int w = 0; w < W16; ++w) {
+        const u32x2 h = {v.x, v.y};
+        __builtin_nontemporal_store(h, static_cast<u32x2*>(a.wr16[w]) + e0 / 4);
+      }
+      if constexpr (W32 + W16 == 0) {
+        if (a.sink_flag) a.sink[0] = v.x ^ v.y ^ v.z ^ v.w;
+      }
+    }
+  }
+}
+
+template <int R32, int R16, int W32, int W16, int ITERS>
+hipError_t launch(const ProbeArgs& a, uint32_t grid, hipStream_t stream) {
+  void* args[] = {const_cast<ProbeArgs*>(&a)};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&probe_kernel<R32, R16, W32, W16, ITERS>), dim3(grid),
+                         dim3(kProbeBlock), args, 0, stream);
+}
+
+// The access shapes of the fused step on the five workloads (g + 2 fp32 reads,
+// P bf16 reads; params and momentum written in fp32, the wire in bf16; 2048-
+// element tiles up to 8 copies, 1024 beyond), their reads alone and writes
+// alone, and a plain copy.
+#define DASO_PROBE_SHAPES(X)                                                   \
+  X(6, 2, 2, 1, 2) X(6, 2, 0, 0, 2) X(0, 0, 2, 1, 2)   /* g=4, P=2  */        \
+  X(6, 4, 2, 1, 2) X(6, 4, 0, 0, 2)                    /* g=4, P=4  */        \
+  X(6, 8, 2, 1, 2) X(6, 8, 0, 0, 2)                    /* g=4, P=8  */        \
+  X(6, 16, 2, 1, 1) X(6, 16, 0, 0, 1) X(0, 0, 2, 1, 1) /* g=4, P=16 */        \
+  X(10, 32, 2, 1, 1) X(10, 32, 0, 0, 1)                /* g=8, P=32 */        \
+  X(1, 0, 1, 0, 2)                                     /* copy      */
+
+}  // namespace
+
+extern "C" {
+
+// Runs one probe: r32/r16 read streams and w32/w16 written streams (host arrays
+// of device pointers, each stream at least n elements of 4 or 2 bytes), tiles of
+// 1024 * iters elements in runs of xcd_run tiles per XCD.  Returns 0, -1 for a
+// shape without an instance or invalid sizes/pointers, -4 when the launch
+// fails.  Nothing is launched on -1.
+int daso_probe_run(const void* const* rd32, int32_t r32, const void* const* rd16, int32_t r16, void* const* wr32,
+                   int32_t w32, void* const* wr16, int32_t w16, uint32_t* sink, int64_t n, int32_t iters,
+                   int32_t xcd_run, hipStream_t stream) {
+  if (n <= 0 || n % 4 != 0 || (iters != 1 && iters != 2) || xcd_run < 1 || sink == nullptr) return -1;
+  if (r32 < 0 || r32 > kMaxRead || r16 < 0 || r16 > kMaxRead || w32 < 0 || w32 > kMaxWrite || w16 < 0 ||
+      w16 > kMaxWrite)
+    return -1;
+  ProbeArgs a = {};
+  for (int i = 0; i < r32; ++i) {
+    if (rd32 == nullptr || rd32[i] == nullptr || (reinterpret_cast<uintptr_t>(rd32[i]) & 15u)) return -1;
+    a.rd32[i] = rd32[i];
+  }
+  for (int i = 0; i < r16; ++i) {
+    if (rd16 == nullptr || rd16[i] == nullptr || (reinterpret_cast<uintptr_t>(rd16[i]) & 15u)) return -1;
+    a.rd16[i] = rd16[i];
+  }
+  for (int i = 0; i < w32; ++i) {
+    if (wr32 == nullptr || wr32[i] == nullptr || (reinterpret_cast<uintptr_t>(wr32[i]) & 15u)) return -1;
+    a.wr32[i] = wr32[i];
+  }
+  for (int i = 0; i < w16; ++i) {
+    if (wr16 == nullptr || wr16[i] == nullptr || (reinterpret_cast<uintptr_t>(wr16[i]) & 15u)) return -1;
+    a.wr16[i] = wr16[i];
+  }
+  const int64_t tile = int64_t(kProbeBlock) * 4 * iters;
+  const int64_t ntiles = (n + tile - 1) / tile;
+  if (ntiles > INT32_MAX) return -1;
+  a.sink = sink;
+  a.n = n;
+  a.ntiles = static_cast<int32_t>(ntiles);
+  a.xcd_run = xcd_run;
+  a.sink_flag = 0;
+  const int64_t block = 8 * int64_t(xcd_run);
+  const int64_t cap = int64_t(1) << 20;
+  const int64_t grid = ntiles <= cap ? ntiles : (block <= cap ? (cap / block) * block : cap);
+#define DASO_PROBE_CASE(A, B, C, D, E)                                                     \
+  if (r32 == (A) && r16 == (B) && w32 == (C) && w16 == (D) && iters == (E))                \
+    return launch<A, B, C, D, E>(a, static_cast<uint32_t>(grid), stream) == hipSuccess ? 0 : -4;
+  DASO_PROBE_SHAPES(DASO_PROBE_CASE)
+#undef DASO_PROBE_CASE
+  return -1;
+}
+
+}  // extern "C"

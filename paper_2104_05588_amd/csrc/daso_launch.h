@@ -99,6 +99,18 @@ struct StatsArgs {
   int32_t nb;
 };
 
+// Workgroups are dispatched to the 8 XCDs of the chip in turn (workgroup w to
+// XCD w % 8).  xcd_runs renumbers workgroup w so that each XCD takes runs of
+// `run` consecutive tiles: the k-th workgroup of XCD x in block b (of 8 * run
+// tiles) gets tile b * 8 * run + x * run + k.  Workgroups past the last whole
+// block keep their number.  A bijection of [0, grid); run = 1 is the identity.
+__device__ __forceinline__ int xcd_runs(int w, int grid, int run) {
+  const int block = 8 * run;
+  if (w >= (grid / block) * block) return w;
+  const int j = w >> 3, x = w & 7;
+  return (j / run) * block + x * run + (j % run);
+}
+
 // Tiles lie on one grid of `tile` elements counted from element 0, so that a
 // wavefront's accesses start on whole cache lines wherever a bucket begins; a
 // bucket [start, end) takes the grid tiles it overlaps, clipped to its range.

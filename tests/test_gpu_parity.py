@@ -511,68 +511,59 @@ def test_fused_workload_full(name):
     compare_fused(got, want, f"workload {name}")
 
 
-def _sample_indices(w, rng, k=1 << 17):
-    idx = set(rng.integers(0, w.n, k).tolist())
-    for b in w.buckets:
-        for d in range(4):
-            idx.update({b.start + d, b.start + b.numel - 1 - d})
-    idx.update({0, w.n - 1})
-    return np.array(sorted(i for i in idx if 0 <= i < w.n), dtype=np.int64)
+def test_fused_gpt_medium_full_size_every_element():
+    """The 354.8M-parameter, g=8, P=32 workload (37 buckets, S = 1/2/4/8 by
+    bucket) at full size, in the launch configuration the bench times (wire and
+    statistics on): inputs are made on the device, the pre-step params and
+    momentum are kept, and after the step every bucket's inputs and outputs are
+    copied to the host and compared element by element with the oracle run on
+    that bucket alone (bit for bit), with the bucket's statistics."""
+    import threading
+    from concurrent.futures import ThreadPoolExecutor
 
-
-def test_fused_gpt_medium_full_size_sampled():
-    """The 354.8M-parameter, g=8, P=32 workload at full size: inputs made on the
-    device; the oracle recomputes sampled elements (every bucket edge plus
-    random positions) one by one, and the per-bucket statistics are checked
-    against fp64 sums of values recomputed with plain torch operations."""
     w = R.workload("gpt_medium")
-    announce("fused gpt_medium full size n=", w.n)
-    torch.manual_seed(0)
+    announce("fused gpt_medium full size, every element: n=", w.n, "buckets=", len(w.buckets))
     inp = Gen.device_inputs(w)
-    rng = np.random.default_rng(41)
-    idx = _sample_indices(w, rng)
-    it = torch.from_numpy(idx).to("cuda")
-    take = lambda t: t.index_select(0, it).cpu().numpy()  # noqa: E731
-    s_grads = [take(t) for t in inp["grads"]]
-    s_stale = [take(t).view(np.uint16) for t in inp["stale"]]
-    s_x, s_m = take(inp["params"]), take(inp["momentum"])
-    x0 = inp["params"].clone()
-    # per-sample buckets, in sample coordinates
-    order = sorted(w.buckets, key=lambda b: b.start)
-    starts = np.array([b.start for b in order])
-    bid = np.searchsorted(starts, idx, side="right") - 1
-    s_bks, i0 = [], 0
-    for i in range(1, len(idx) + 1):
-        if i == len(idx) or bid[i] != bid[i0]:
-            s_bks.append((i0, i - i0, order[bid[i0]].S))
-            i0 = i
+    x0, m0 = inp["params"].clone(), inp["momentum"].clone()
     bks = [(b.start, b.numel, b.S) for b in w.buckets]
     wire = torch.empty(w.n, dtype=torch.int16, device="cuda")
     st = daso.new_stats(len(bks))
     daso.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks,
                          w.lr, w.mu, w.wd, wire, None, st)
     torch.cuda.synchronize()
-    want = O.fused_sync_step(s_grads, s_x, s_m, s_stale, s_bks, w.lr, w.mu, w.wd)
-    check_f32(take(inp["params"]), want["params"], "gpt sampled params")
-    check_f32(take(inp["momentum"]), want["momentum"], "gpt sampled momentum")
-    check_u16(take(wire).view(np.uint16), want["wire"], "gpt sampled wire")
+    got_stats = daso.decode_stats(st)
 
-    # statistics: fp64 sums of gbar^2 and (x' - xl)^2 per bucket
-    got = daso.decode_stats(st)
-    gsum = inp["grads"][0].clone()
-    for t in inp["grads"][1:]:
-        gsum += t
-    gbar = gsum / float(w.g)
-    del gsum
-    lr_t = torch.tensor(w.lr, dtype=torch.float32, device="cuda")
-    xl = x0 - torch.mul(inp["momentum"], lr_t)
-    for b, bk in enumerate(w.buckets):
-        sl = slice(bk.start, bk.start + bk.numel)
-        gsq = float(torch.sum(gbar[sl].double() ** 2))
-        dsq = float(torch.sum((inp["params"][sl].double() - xl[sl].double()) ** 2))
-        assert abs(got[b][0] - gsq) <= 1e-9 * gsq, (b, got[b], gsq)
-        assert abs(got[b][1] - dsq) <= 1e-9 * dsq, (b, got[b], dsq)
-        assert got[b][2] == 0
+    def check_bucket(b, part):
+        want = O.fused_sync_step(part["grads"], part["x0"], part["m0"], part["stale"], [(0, part["k"], part["S"])],
+                                 w.lr, w.mu, w.wd)
+        what = f"gpt_medium bucket {b} (start {w.buckets[b].start}, {part['k']} elements, S={part['S']})"
+        check_f32(part["params"], want["params"], what + " params")
+        check_f32(part["momentum"], want["momentum"], what + " momentum")
+        check_u16(part["wire"], want["wire"], what + " wire")
+        check_stats([got_stats[b]], want["stats"], what + " stats")
+        return part["k"]
+
+    # the device-to-host copies run here, the oracle in worker threads (numpy
+    # releases the GIL); at most 6 buckets are held on the host at once
+    slots = threading.Semaphore(6)
+    futures = []
+    with ThreadPoolExecutor(8) as ex:
+        for b, bk in enumerate(w.buckets):
+            sl = slice(bk.start, bk.start + bk.numel)
+            slots.acquire()
+            part = {"k": bk.numel, "S": bk.S, "grads": [host_f32(t[sl]) for t in inp["grads"]],
+                    "stale": [host_u16(t[sl]) for t in inp["stale"]], "x0": host_f32(x0[sl]),
+                    "m0": host_f32(m0[sl]), "params": host_f32(inp["params"][sl]),
+                    "momentum": host_f32(inp["momentum"][sl]), "wire": host_u16(wire[sl])}
+
+            def job(b=b, part=part):
+                try:
+                    return check_bucket(b, part)
+                finally:
+                    slots.release()
+            futures.append(ex.submit(job))
+        checked = sum(f.result() for f in futures)
+    assert checked == w.n
 
 
 # ------------------------------------------------------------ fp32 exchange
