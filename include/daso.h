@@ -97,6 +97,8 @@ extern "C" {
 #define DASO_EALIGN (-2)  /* a device base pointer is not 16-byte aligned */
 #define DASO_EALIAS (-3)  /* an output overlaps an input other than in the allowed in-place pairs */
 #define DASO_EHIP (-4)    /* a HIP call (launch, allocation of the stats workspace) failed */
+#define DASO_ENOSPACE (-5) /* daso_fused_sync_step_noalloc: the statistics need more than
+                              DASO_NOALLOC_SCRATCH_BYTES of scratch */
 
 #define DASO_MAX_G 64     /* most replica gradients per call */
 #define DASO_MAX_P 64     /* most exchanged copies per call */
@@ -193,6 +195,26 @@ int daso_global_merge_f32(float* params, const float* const* stale, int32_t P,
  * buffer; wire, stats and grad_avg (apart from the allowed grads alias) must not
  * overlap anything else; inputs may overlap each other. */
 int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): daso_fused_sync_step
+ * with the same arguments, results and rules, except that the statistics
+ * scratch (24 bytes per tile of 1024 or 2048 parameters plus a 260-byte table,
+ * per launch of up to 64 buckets) lives in a fixed array of
+ * DASO_NOALLOC_SCRATCH_BYTES in device memory instead of an allocated
+ * workspace.  The call never allocates or frees memory.  Every GPU the library
+ * runs on holds its own copy of that array until the process ends; the first
+ * call on a device looks up its address there (that device must be current, as
+ * for every call).  All calls of this entry point on one GPU share the array and
+ * each leaves its contents behind: calls queued on one stream are ordered by it
+ * (host threads may share the stream), but calls on different streams of the
+ * same GPU that may run at the same time race on the array and can give wrong
+ * statistics; the other outputs are never affected.  A call whose statistics
+ * need more than the array holds (more than 699,039 tiles in one launch: at
+ * least about 715 million parameters) returns DASO_ENOSPACE and launches
+ * nothing.  Without statistics (stats == NULL) no scratch is used. */
+#define DASO_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int daso_fused_sync_step_noalloc(const daso_sync_args* args, hipStream_t stream);
 
 /* Bucket plan for a flat parameter buffer (host only, no device work).  The
  * tensors of a model lie end to end in forward order with element counts

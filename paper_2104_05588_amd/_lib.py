@@ -21,13 +21,14 @@ DASO_EINVAL = -1
 DASO_EALIGN = -2
 DASO_EALIAS = -3
 DASO_EHIP = -4
+DASO_ENOSPACE = -5
 DASO_MAX_G = 64
 DASO_MAX_P = 64
 DASO_PACK_PRE_MERGE = 1
 DASO_EXCHANGE_F32 = 2
 
 EXPORTED = ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
-            "daso_fused_sync_step", "daso_plan_buckets", "daso_schedule_create", "daso_schedule_next",
+            "daso_fused_sync_step", "daso_fused_sync_step_noalloc", "daso_plan_buckets", "daso_schedule_create", "daso_schedule_next",
             "daso_schedule_end_epoch", "daso_schedule_destroy", "daso_status_string", "daso_abi_version")
 BUCKET_CAP_ELEMS = 25 * 1024 * 1024 // 4  # 25 MiB of fp32
 
@@ -81,6 +82,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                       vp, i64, vp]
     lib.daso_global_merge_f32.argtypes = lib.daso_global_merge.argtypes
     lib.daso_fused_sync_step.argtypes = [ctypes.POINTER(daso_sync_args), vp]
+    lib.daso_fused_sync_step_noalloc.argtypes = [ctypes.POINTER(daso_sync_args), vp]
     lib.daso_plan_buckets.argtypes = [ctypes.POINTER(i64), i32, i64, ctypes.POINTER(i32), i32,
                                       ctypes.POINTER(daso_bucket), i32]
     lib.daso_plan_buckets.restype = i32
@@ -88,7 +90,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.daso_status_string.restype = ctypes.c_char_p
     lib.daso_abi_version.argtypes = []
     for name in ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
-                 "daso_fused_sync_step", "daso_abi_version"):
+                 "daso_fused_sync_step", "daso_fused_sync_step_noalloc", "daso_abi_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -220,13 +222,15 @@ def decode_stats(stats: torch.Tensor) -> List[Tuple[float, float, int]]:
 class FusedStep:
     """A prepared daso_fused_sync_step: argument checks and marshalling happen
     once here, so that each call costs one C call.  The tensors must stay alive
-    (and keep their storage) while the object is used."""
+    (and keep their storage) while the object is used.  noalloc=True calls
+    daso_fused_sync_step_noalloc instead (statistics scratch in the library's
+    fixed device array: no allocation, DasoError with DASO_ENOSPACE beyond it)."""
 
     def __init__(self, grads: Sequence[torch.Tensor], params: torch.Tensor, momentum: torch.Tensor,
                  stale: Sequence[torch.Tensor], buckets: Sequence[Tuple[int, int, int]],
                  lr: float, mu: float, weight_decay: float = 0.0, wire: Optional[torch.Tensor] = None,
                  grad_avg: Optional[torch.Tensor] = None, stats: Optional[torch.Tensor] = None,
-                 flags: int = 0):
+                 flags: int = 0, noalloc: bool = False):
         n = params.numel()
         self._keep = (list(grads), params, momentum, list(stale), wire, grad_avg, stats)
         f32 = _is_f32_exchange(stale, wire)
@@ -261,21 +265,23 @@ class FusedStep:
         a.stats = stats.data_ptr() if stats is not None else None
         self.args = a
         self._byref = ctypes.byref(a)
-        self._fn = load().daso_fused_sync_step
+        self._name = "daso_fused_sync_step_noalloc" if noalloc else "daso_fused_sync_step"
+        self._fn = getattr(load(), self._name)
 
     def __call__(self, stream=None) -> None:
         if torch.cuda.current_device() != self._device:
             raise ValueError(f"prepared on cuda:{self._device}, called with cuda:{torch.cuda.current_device()} "
                              "current")
-        _check(self._fn(self._byref, _stream_handle(stream)), "daso_fused_sync_step")
+        _check(self._fn(self._byref, _stream_handle(stream)), self._name)
 
 
 def fused_sync_step(grads, params, momentum, stale, buckets, lr, mu, weight_decay=0.0, wire=None,
-                    grad_avg=None, stats=None, flags=0, stream=None) -> None:
+                    grad_avg=None, stats=None, flags=0, stream=None, noalloc=False) -> None:
     """One DASO synchronisation step (see include/daso.h), in place on params
-    and momentum; writes wire, grad_avg and stats when given."""
+    and momentum; writes wire, grad_avg and stats when given.  noalloc=True
+    uses daso_fused_sync_step_noalloc."""
     FusedStep(grads, params, momentum, stale, buckets, lr, mu, weight_decay, wire, grad_avg, stats,
-              flags)(stream)
+              flags, noalloc)(stream)
 
 
 # ------------------------------------------------- phase/schedule controller

@@ -60,6 +60,38 @@ int reserve(Workspace& w, size_t need) {
   return DASO_OK;
 }
 
+// ---------------------------------------------------------- fixed scratch
+// The statistics scratch of daso_fused_sync_step_noalloc: one array of fixed
+// size in device memory, of which every GPU the library runs on holds its own
+// copy until the process ends.  In host code `scratch` names a host-side stand-in,
+// not device memory: the device address is looked up once per device with
+// hipGetSymbolAddress (with that device current) and only that address is
+// handed to kernels.  The kernels write every partial and table entry they read
+// later, so the array never needs clearing.
+constexpr size_t kScratchBytes = DASO_NOALLOC_SCRATCH_BYTES;
+static_assert(kScratchBytes % 256 == 0, "the scratch size is a whole number of 256-byte blocks");
+static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)];
+
+constexpr int kMaxDevices = 64;
+
+struct ScratchSlot {
+  std::once_flag once;
+  hipError_t err = hipSuccess;
+  void* ptr = nullptr;
+  std::mutex mu;  // held by a call from choosing the buffer until its last launch is queued
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+// The device address of `scratch` on device `dev`, which must be current.
+int scratch_slot(int dev, ScratchSlot** out) {
+  if (dev < 0 || dev >= kMaxDevices) return DASO_EHIP;
+  ScratchSlot& s = g_scratch[dev];
+  std::call_once(s.once, [&s] { s.err = hipGetSymbolAddress(&s.ptr, HIP_SYMBOL(scratch)); });
+  if (s.err != hipSuccess || s.ptr == nullptr) return DASO_EHIP;
+  *out = &s;
+  return DASO_OK;
+}
+
 // -------------------------------------------------------------- launching
 struct Group {
   int32_t first;  // index of its first bucket in the caller's table
@@ -121,11 +153,14 @@ int current_device(hipStream_t stream, int* dev) {
   return sdev == *dev ? DASO_OK : DASO_EINVAL;
 }
 
+// Where a fused launch with statistics keeps its tile partials and table.
+enum class Space {
+  kAllocated,  // the per-(device, stream) workspace, allocated on first use
+  kFixed,      // the fixed `scratch` array; calls needing more fail with DASO_ENOSPACE
+};
+
 int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
-               daso_bucket_stats* stats, hipStream_t stream) {
-  int dev = 0;
-  const int drc = current_device(stream, &dev);
-  if (drc != DASO_OK) return drc;
+               daso_bucket_stats* stats, hipStream_t stream, Space space = Space::kAllocated) {
   const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
   const int64_t tile = daso::tile_elems(mode, with_stats, a);
   const std::vector<Group> groups = group_buckets(b, nb, tile);
@@ -134,6 +169,13 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     if (gr.ntiles > INT32_MAX) return DASO_EINVAL;
     max_tiles = std::max(max_tiles, gr.ntiles);
   }
+  // statistics scratch: tile partials, then the table of bucket tile ranges
+  const size_t table_at = static_cast<size_t>(max_tiles) * sizeof(TilePartial);
+  const size_t need = table_at + (daso::kLaunchBuckets + 1) * sizeof(int32_t);
+  if (with_stats && space == Space::kFixed && need > kScratchBytes) return DASO_ENOSPACE;
+  int dev = 0;
+  const int drc = current_device(stream, &dev);
+  if (drc != DASO_OK) return drc;
   // tile order across the XCDs, by the number of streams the launch touches
   // (the measured rule is stated with the constants in daso_launch.h)
   int streams = 2;
@@ -147,13 +189,22 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     a.xcd_run = static_cast<int32_t>(std::max<int64_t>(1, fused_run_elems() / tile));
   std::unique_lock<std::mutex> hold;
   if (with_stats) {
-    Workspace& w = workspace_entry(dev, stream);
-    hold = std::unique_lock<std::mutex>(w.mu);
-    const size_t table_at = static_cast<size_t>(max_tiles) * sizeof(TilePartial);
-    const int rc = reserve(w, table_at + (daso::kLaunchBuckets + 1) * sizeof(int32_t));
-    if (rc != DASO_OK) return rc;
-    a.partials = static_cast<TilePartial*>(w.ptr);
-    a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(w.ptr) + table_at);
+    void* base = nullptr;
+    if (space == Space::kFixed) {
+      ScratchSlot* slot = nullptr;
+      const int rc = scratch_slot(dev, &slot);
+      if (rc != DASO_OK) return rc;
+      hold = std::unique_lock<std::mutex>(slot->mu);
+      base = slot->ptr;
+    } else {
+      Workspace& w = workspace_entry(dev, stream);
+      hold = std::unique_lock<std::mutex>(w.mu);
+      const int rc = reserve(w, need);
+      if (rc != DASO_OK) return rc;
+      base = w.ptr;
+    }
+    a.partials = static_cast<TilePartial*>(base);
+    a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(base) + table_at);
   }
   for (const auto& gr : groups) {
     fill_group(a, b, gr, tile);
@@ -225,7 +276,11 @@ int daso_global_merge_f32(float* params, const float* const* stale, int32_t P, c
   return merge_impl(params, reinterpret_cast<const void* const*>(stale), P, buckets, nbuckets, wire, n, 4, stream);
 }
 
-int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+int fused_impl(const daso_sync_args* args, hipStream_t stream, Space space) {
   if (args == nullptr) return DASO_EINVAL;
   const daso_sync_args& s = *args;
   daso::host::FusedView v;
@@ -246,7 +301,19 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
   a.wd = s.weight_decay;
   a.flags = s.flags;
   a.xf32 = v.xf32 ? 1 : 0;
-  return run_groups(daso::kModeFused, a, s.buckets, s.nbuckets, s.stats, stream);
+  return run_groups(daso::kModeFused, a, s.buckets, s.nbuckets, s.stats, stream, space);
+}
+
+}  // namespace
+
+extern "C" {
+
+int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
+  return fused_impl(args, stream, Space::kAllocated);
+}
+
+int daso_fused_sync_step_noalloc(const daso_sync_args* args, hipStream_t stream) {
+  return fused_impl(args, stream, Space::kFixed);
 }
 
 }  // extern "C"

@@ -162,7 +162,7 @@ int64_t launch_grid(int64_t ntiles, int32_t run) {
 
 extern "C" {
 
-int daso_abi_version(void) { return 100; }
+int daso_abi_version(void) { return 101; }
 
 int32_t daso_plan_buckets(const int64_t* numels, int32_t ntensors, int64_t cap_elems, const int32_t* S_cycle,
                           int32_t n_cycle, daso_bucket* out, int32_t out_cap) {
@@ -203,6 +203,9 @@ const char* daso_status_string(int status) {
     case DASO_EALIGN: return "DASO_EALIGN: a device buffer is not 16-byte aligned";
     case DASO_EALIAS: return "DASO_EALIAS: an output buffer overlaps another buffer";
     case DASO_EHIP: return "DASO_EHIP: a HIP call failed";
+    case DASO_ENOSPACE:
+      return "DASO_ENOSPACE: the statistics need more scratch than the fixed array of "
+             "daso_fused_sync_step_noalloc holds (DASO_NOALLOC_SCRATCH_BYTES: 24 bytes per tile plus 260)";
     default: return "unknown DASO status";
   }
 }

@@ -45,8 +45,8 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_status_strings_and_version(lib):
-    assert lib.daso_abi_version() == 100
-    for code in (L.DASO_OK, L.DASO_EINVAL, L.DASO_EALIGN, L.DASO_EALIAS, L.DASO_EHIP):
+    assert lib.daso_abi_version() == 101
+    for code in (L.DASO_OK, L.DASO_EINVAL, L.DASO_EALIGN, L.DASO_EALIAS, L.DASO_EHIP, L.DASO_ENOSPACE):
         s = L.status_string(code)
         assert s.startswith("DASO_")
     assert "unknown" in L.status_string(-99)
@@ -161,9 +161,10 @@ def _args(n=1000, g=2, P=2):
     return a, keep
 
 
-def test_fused_rejects(lib):
+@pytest.mark.parametrize("entry", ["daso_fused_sync_step", "daso_fused_sync_step_noalloc"])
+def test_fused_rejects(lib, entry):
     _no_gpu()
-    f = lib.daso_fused_sync_step
+    f = getattr(lib, entry)
     assert f(None, None) == L.DASO_EINVAL
 
     def rc(**kw):
@@ -197,6 +198,37 @@ def test_fused_rejects(lib):
     assert rc(flags=L.DASO_EXCHANGE_F32, stale=None, wire=None,
               stale_f32=st32, wire_f32=A + 30 * MB + 8) == L.DASO_EALIGN
     assert rc(flags=L.DASO_EXCHANGE_F32, stale=None, wire=None, n=0, stale_f32=st32) == L.DASO_OK
+
+
+def test_noalloc_rejects_statistics_beyond_its_scratch(lib):
+    """daso_fused_sync_step_noalloc keeps the statistics partials (24 bytes per
+    tile) and the 65-entry table of a launch in its fixed 16 MiB array: 699,039
+    tiles fit, one more is DASO_ENOSPACE before any HIP call.  g = 1, P = 0 runs
+    2048-element tiles.  Without statistics there is no limit; with room the
+    call goes on to HIP, which fails here without a GPU."""
+    _no_gpu()
+    f = lib.daso_fused_sync_step_noalloc
+    GB8 = 8 << 30
+    assert L.DASO_ENOSPACE == -5 and "DASO_ENOSPACE" in L.status_string(L.DASO_ENOSPACE)
+    fit = 699_039
+
+    def rc(n, stats=True, nb=1):
+        a = L.daso_sync_args()
+        keep = [ptrs(A), L.bucket_table([(0, n, 1)] if nb == 1 else [(0, n - 5, 1), (n - 5, 5, 2)])]
+        a.n, a.g, a.P = n, 1, 0
+        a.grads, a.stale = keep[0], None
+        a.params, a.momentum, a.wire = A + GB8, A + 2 * GB8, A + 3 * GB8
+        a.stats = A + 4 * GB8 if stats else None
+        a.buckets, a.nbuckets = keep[1], nb
+        a.lr, a.mu = 0.1, 0.9
+        return f(ctypes.byref(a), None)
+
+    assert (24 * fit + 65 * 4) <= (16 << 20) < 24 * (fit + 1) + 65 * 4
+    assert rc(fit * 2048 + 1) == L.DASO_ENOSPACE
+    assert rc(fit * 2048 + 1, nb=2) == L.DASO_ENOSPACE
+    assert rc(fit * 2048) == L.DASO_EHIP
+    assert rc(fit * 2048 + 1, stats=False) == L.DASO_EHIP
+    assert lib.daso_fused_sync_step(ctypes.byref(L.daso_sync_args()), None) == L.DASO_EINVAL
 
 
 def test_global_merge_f32_rejects(lib):

@@ -1,0 +1,103 @@
+"""daso_fused_sync_step_noalloc (statistics scratch in the library's fixed device
+array, no allocation) against daso_fused_sync_step on the same inputs: every
+output bit for bit, on two calls in a row, the second one smaller, so that the
+second call runs over partials the first left in the shared array."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2104_05588_amd as daso
+from workloads import generate as Gen
+from workloads import recipes as R
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    daso.load()
+    yield
+    torch.cuda.synchronize()
+
+
+def _random_case(seed, n, g, P, nb):
+    rng = np.random.default_rng(seed)
+    x = (rng.standard_normal(n) * 0.02).astype(F32)
+    host = {"params": x, "momentum": (rng.standard_normal(n) * 1e-3).astype(F32),
+            "grads": [(rng.standard_normal(n) * 1e-3).astype(F32) for _ in range(g)],
+            "stale": [(torch.from_numpy(x + (rng.standard_normal(n) * 1e-4).astype(F32))
+                       .to(torch.bfloat16).view(torch.int16)) for _ in range(P)]}
+    cuts = sorted(set(rng.integers(1, n, nb - 1).tolist()))
+    edges = [0] + cuts + [n]
+    bks = [(edges[i], edges[i + 1] - edges[i], int(rng.choice([0, 1, 2, 4, 8]))) for i in range(len(edges) - 1)]
+    bks = [bks[i] for i in rng.permutation(len(bks))]
+    dev = {"params": torch.from_numpy(host["params"]).cuda(), "momentum": torch.from_numpy(host["momentum"]).cuda(),
+           "grads": [torch.from_numpy(a).cuda() for a in host["grads"]],
+           "stale": [t.cuda() for t in host["stale"]]}
+    return dev, bks
+
+
+def _workload_case(name):
+    w = R.workload(name)
+    return Gen.device_inputs(w), [(b.start, b.numel, b.S) for b in w.buckets]
+
+
+def _run(inp, bks, noalloc):
+    """One fused step on copies of the inputs; returns the outputs on the host."""
+    n = inp["params"].numel()
+    x, m = inp["params"].clone(), inp["momentum"].clone()
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    stats = daso.new_stats(len(bks))
+    daso.fused_sync_step(inp["grads"], x, m, inp["stale"], bks, 0.1, 0.9, 0.0, wire, None, stats,
+                         noalloc=noalloc)
+    torch.cuda.synchronize()
+    return {"params": x.cpu().numpy().view(np.uint32), "momentum": m.cpu().numpy().view(np.uint32),
+            "wire": wire.cpu().numpy().view(np.uint16), "stats": stats.cpu().numpy().view(np.uint64)}
+
+
+def _same(a, b, what):
+    for k in ("params", "momentum", "wire", "stats"):
+        diff = np.count_nonzero(a[k] != b[k])
+        assert diff == 0, f"{what}: {k} differs in {diff} of {a[k].size} entries"
+
+
+@pytest.mark.parametrize("first,second", [
+    ("resnet50", "tiny"),                                  # full workload shapes, the bench's call first
+    ((1, 1_000_003, 4, 8, 5), (2, 70_001, 3, 5, 3)),       # node shape, then a bounded instance
+    ((3, 600_001, 8, 32, 7), (4, 4097, 9, 40, 2)),         # 1024-element tiles, then the run-time-count path
+])
+def test_noalloc_matches_fused_step_on_two_calls(first, second):
+    cases = []
+    for spec in (first, second):
+        print(f"\n[case] noalloc vs fused: {spec}", flush=True)
+        inp, bks = _workload_case(spec) if isinstance(spec, str) else _random_case(*spec)
+        n = inp["params"].numel()
+        cases.append((inp, bks, n))
+    assert cases[1][2] < cases[0][2]
+    # both calls of the fixed-scratch entry point back to back, then the reference calls
+    got = [_run(inp, bks, noalloc=True) for inp, bks, _ in cases]
+    for (inp, bks, n), g in zip(cases, got):
+        want = _run(inp, bks, noalloc=False)
+        _same(g, want, f"n={n} buckets={len(bks)}")
+
+
+def test_noalloc_without_statistics_and_on_a_side_stream():
+    inp, bks = _random_case(5, 300_007, 4, 4, 4)
+    n = inp["params"].numel()
+    want = _run(inp, bks, noalloc=False)
+    x, m = inp["params"].clone(), inp["momentum"].clone()
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        daso.fused_sync_step(inp["grads"], x, m, inp["stale"], bks, 0.1, 0.9, 0.0, wire, None, None,
+                             noalloc=True)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert np.array_equal(x.cpu().numpy().view(np.uint32), want["params"])
+    assert np.array_equal(m.cpu().numpy().view(np.uint32), want["momentum"])
+    assert np.array_equal(wire.cpu().numpy().view(np.uint16), want["wire"])
