@@ -70,7 +70,7 @@ class Probes:
         self.lib = ctypes.CDLL(PROBE_LIB)
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         self.lib.daso_probe_run.argtypes = [ctypes.POINTER(vp), i32, ctypes.POINTER(vp), i32, ctypes.POINTER(vp),
-                                            i32, ctypes.POINTER(vp), i32, vp, i64, i32, i32, vp]
+                                            i32, ctypes.POINTER(vp), i32, vp, i64, i32, i32, i32, vp]
         self.lib.daso_probe_run.restype = ctypes.c_int
         self.sink = torch.zeros(4, dtype=torch.int32, device="cuda")
 
@@ -82,11 +82,11 @@ class Probes:
             arr[i] = t.data_ptr()
         return arr
 
-    def call(self, rd32, rd16, wr32, wr16, n, iters, xcd_run):
+    def call(self, rd32, rd16, wr32, wr16, n, iters, xcd_run, lds=0):
         """A callable that launches the probe once on the current stream."""
         args = (self._arr(rd32, n, 4), len(rd32), self._arr(rd16, n, 2), len(rd16), self._arr(wr32, n, 4),
                 len(wr32), self._arr(wr16, n, 2), len(wr16), self.ct.c_void_p(self.sink.data_ptr()),
-                self.ct.c_int64(n), iters, xcd_run)
+                self.ct.c_int64(n), iters, xcd_run, lds)
         keep = (rd32, rd16, wr32, wr16)
         torch = self.torch
 
@@ -96,22 +96,6 @@ class Probes:
             if rc != 0:
                 raise RuntimeError(f"daso_probe_run failed with {rc}")
         return run
-
-
-def step_tile_and_run(g: int, P: int, wire: bool = True):
-    """Tile size and XCD run length the library takes for a fused step with bf16
-    copies and g, P at a node shape (the rule stated in daso_launch.h): tiles of
-    2048 elements when a vector's inputs take at most 48 registers (4g + 2P + 8),
-    else 1024; runs of 32 tiles from 32 streams, 16 from 20, 32K elements from 9."""
-    tile = 2048 if 4 * g + 2 * P + 8 <= 48 else 1024
-    streams = g + P + 4 + (1 if wire else 0)
-    if streams >= 32:
-        return tile, 32
-    if streams >= 20:
-        return tile, 16
-    if streams >= 9:
-        return tile, max(1, 32768 // tile)
-    return tile, 1
 
 
 def time_cold(torch, fn, reps, scratch):
@@ -157,13 +141,14 @@ def copy_rate(torch, probes, reps=10):
 
 
 def ceiling(torch, probes, w, inp, wire, step, reps):
-    """The step and its access pattern on the step's own buffers, tile grid and
-    tile order, each cold (cache evicted before every call) and warm (back to
+    """The step and its access pattern on the step's own buffers, tile grid, tile
+    order and occupancy cap, each cold (cache evicted before every call) and warm (back to
     back): the reads alone (g + 2 fp32 and P bf16 streams), the writes alone
     (params and momentum fp32, the wire bf16), both mixed as a bare kernel, and
     the separated bound = reads alone + writes alone."""
     n = w.n
-    tile, run = step_tile_and_run(w.g, w.P)
+    cfg = step.launch_config()  # the step's own tile size, tile order and occupancy cap
+    tile, run, lds = cfg["tile_elems"], cfg["xcd_run_tiles"], cfg["lds_bytes"]
     it = tile // 1024
     rd32 = list(inp["grads"]) + [inp["params"], inp["momentum"]]
     rd16 = list(inp["stale"])
@@ -172,10 +157,11 @@ def ceiling(torch, probes, w, inp, wire, step, reps):
     write_b = n * 10
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     fns = {"step": step,
-           "reads_alone": probes.call(rd32, rd16, [], [], n, it, run),
-           "writes_alone": probes.call([], [], wr32, wr16, n, it, run),
-           "bare_mix": probes.call(rd32, rd16, wr32, wr16, n, it, run)}
-    out = {"tile_elems": tile, "xcd_run_tiles": run, "read_bytes": read_b, "write_bytes": write_b}
+           "reads_alone": probes.call(rd32, rd16, [], [], n, it, run, lds),
+           "writes_alone": probes.call([], [], wr32, wr16, n, it, run, lds),
+           "bare_mix": probes.call(rd32, rd16, wr32, wr16, n, it, run, lds)}
+    out = {"tile_elems": tile, "xcd_run_tiles": run, "lds_bytes": lds, "read_bytes": read_b,
+           "write_bytes": write_b}
     for name, fn in fns.items():
         med, mn = time_cold(torch, fn, reps, scratch)
         out[name] = {"cold_median_us": med, "cold_min_us": mn, "warm_us": time_warm(torch, fn, reps)}

@@ -60,11 +60,13 @@
  *    queueing one of them fails (DASO_EHIP), the kernels queued before it still
  *    run: the outputs (params, momentum, wire, grad_avg, stats) of the buckets
  *    they cover may then already be updated, the others are untouched.
- *  - Tile order: the fused step hands each XCD runs of consecutive tiles whose
- *    length was measured best on MI355X (32768 elements below 20 streams).  The
- *    environment variable DASO_FUSED_RUN_ELEMS (read once per process; 0 =
- *    plain order) replaces that length, to reproduce the measurement.  The
- *    order never changes a result.
+ *  - Launch shape: the fused step hands each XCD runs of consecutive tiles
+ *    (about 64 blocks of 8 runs per launch from 9 streams) and, from 10
+ *    streams, lets at most 2 workgroups share a CU; both were measured best on
+ *    MI355X (daso_fused_launch_config reports them).  The environment variables
+ *    DASO_FUSED_RUN_ELEMS (elements per run, 0 = plain order) and
+ *    DASO_FUSED_WG_PER_CU (0 = no cap), read once per process, replace them to
+ *    reproduce the measurements.  Neither ever changes a result.
  *  - Calls may be made from several host threads.  Fused steps with statistics
  *    share one small per-(device, stream) workspace (24 bytes per tile of 1024
  *    or 2048 parameters, plus a 260-byte table of bucket ranges) that the
@@ -215,6 +217,23 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
  * nothing.  Without statistics (stats == NULL) no scratch is used. */
 #define DASO_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
 int daso_fused_sync_step_noalloc(const daso_sync_args* args, hipStream_t stream);
+
+/* Launch shape of a fused step (host only, no device work), for tools that
+ * time the same memory access pattern: daso_fused_sync_step and
+ * daso_fused_sync_step_noalloc with these arguments run tiles of tile_elems
+ * parameters, one 256-thread workgroup per tile, hand each XCD runs of
+ * xcd_run_tiles consecutive tiles (1: plain order), and give each workgroup
+ * lds_bytes of LDS (unused by the kernel; it caps how many workgroups share a
+ * CU; 0: no cap).  ntiles counts the tiles of the first launch (the first 64
+ * buckets).  The arguments are checked as the step checks them and the same
+ * status is returned; *out is written only on DASO_OK. */
+typedef struct daso_launch_config {
+  int64_t tile_elems;
+  int64_t ntiles;
+  int32_t xcd_run_tiles;
+  int32_t lds_bytes;
+} daso_launch_config;
+int daso_fused_launch_config(const daso_sync_args* args, daso_launch_config* out);
 
 /* Bucket plan for a flat parameter buffer (host only, no device work).  The
  * tensors of a model lie end to end in forward order with element counts

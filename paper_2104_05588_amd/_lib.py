@@ -28,7 +28,8 @@ DASO_PACK_PRE_MERGE = 1
 DASO_EXCHANGE_F32 = 2
 
 EXPORTED = ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
-            "daso_fused_sync_step", "daso_fused_sync_step_noalloc", "daso_plan_buckets", "daso_schedule_create", "daso_schedule_next",
+            "daso_fused_sync_step", "daso_fused_sync_step_noalloc", "daso_fused_launch_config",
+            "daso_plan_buckets", "daso_schedule_create", "daso_schedule_next",
             "daso_schedule_end_epoch", "daso_schedule_destroy", "daso_status_string", "daso_abi_version")
 BUCKET_CAP_ELEMS = 25 * 1024 * 1024 // 4  # 25 MiB of fp32
 
@@ -54,6 +55,11 @@ class daso_sync_args(ctypes.Structure):
         ("flags", ctypes.c_uint32), ("stats", ctypes.c_void_p),
         ("stale_f32", ctypes.POINTER(ctypes.c_void_p)), ("wire_f32", ctypes.c_void_p),
     ]
+
+
+class daso_launch_config(ctypes.Structure):
+    _fields_ = [("tile_elems", ctypes.c_int64), ("ntiles", ctypes.c_int64),
+                ("xcd_run_tiles", ctypes.c_int32), ("lds_bytes", ctypes.c_int32)]
 
 
 class DasoError(RuntimeError):
@@ -83,6 +89,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.daso_global_merge_f32.argtypes = lib.daso_global_merge.argtypes
     lib.daso_fused_sync_step.argtypes = [ctypes.POINTER(daso_sync_args), vp]
     lib.daso_fused_sync_step_noalloc.argtypes = [ctypes.POINTER(daso_sync_args), vp]
+    lib.daso_fused_launch_config.argtypes = [ctypes.POINTER(daso_sync_args), ctypes.POINTER(daso_launch_config)]
     lib.daso_plan_buckets.argtypes = [ctypes.POINTER(i64), i32, i64, ctypes.POINTER(i32), i32,
                                       ctypes.POINTER(daso_bucket), i32]
     lib.daso_plan_buckets.restype = i32
@@ -90,7 +97,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.daso_status_string.restype = ctypes.c_char_p
     lib.daso_abi_version.argtypes = []
     for name in ("daso_local_avg", "daso_pack_bf16", "daso_global_merge", "daso_global_merge_f32",
-                 "daso_fused_sync_step", "daso_fused_sync_step_noalloc", "daso_abi_version"):
+                 "daso_fused_sync_step", "daso_fused_sync_step_noalloc", "daso_fused_launch_config",
+                 "daso_abi_version"):
         getattr(lib, name).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -267,6 +275,13 @@ class FusedStep:
         self._byref = ctypes.byref(a)
         self._name = "daso_fused_sync_step_noalloc" if noalloc else "daso_fused_sync_step"
         self._fn = getattr(load(), self._name)
+
+    def launch_config(self) -> dict:
+        """The launch shape of this call (daso_fused_launch_config): elements per
+        tile, tiles of the first launch, tiles per XCD run, LDS per workgroup."""
+        c = daso_launch_config()
+        _check(load().daso_fused_launch_config(self._byref, ctypes.byref(c)), "daso_fused_launch_config")
+        return {f: getattr(c, f) for f, _ in daso_launch_config._fields_}
 
     def __call__(self, stream=None) -> None:
         if torch.cuda.current_device() != self._device:

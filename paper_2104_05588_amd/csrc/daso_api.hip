@@ -127,20 +127,60 @@ void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr, int64_t tile
   a.ntiles = static_cast<int32_t>(std::max<int64_t>(t, 1));
 }
 
-// DASO_FUSED_RUN_ELEMS, when set to a non-negative number of elements, replaces
-// the measured run length of the fused step below kXcdRunMidStreams streams
-// (0: plain order).  The tile order never changes a result; the variable
-// exists to reproduce the measurements behind the default.  Read once.
-int64_t fused_run_elems() {
-  static const int64_t v = [] {
-    const char* e = getenv("DASO_FUSED_RUN_ELEMS");
-    if (e == nullptr || *e == '\0') return daso::kXcdRunFusedElems;
-    char* end = nullptr;
-    const long long x = strtoll(e, &end, 10);
-    return (end != e && *end == '\0' && x >= 0 && x <= (1LL << 30)) ? static_cast<int64_t>(x)
-                                                                    : daso::kXcdRunFusedElems;
-  }();
+// A non-negative integer from the environment, read once per variable by the
+// caller's static; `fallback` when unset, malformed or above `max`.
+int64_t env_count(const char* name, int64_t fallback, int64_t max) {
+  const char* e = getenv(name);
+  if (e == nullptr || *e == '\0') return fallback;
+  char* end = nullptr;
+  const long long x = strtoll(e, &end, 10);
+  return (end != e && *end == '\0' && x >= 0 && x <= max) ? static_cast<int64_t>(x) : fallback;
+}
+
+// DASO_FUSED_RUN_ELEMS, when set to a number of elements, replaces the run
+// length of fused launches of kXcdRunFusedStreams streams or more (0: plain
+// order); DASO_FUSED_WG_PER_CU, when set, replaces the workgroups-per-CU cap of
+// fused launches of kCapStreams streams or more (0: no cap).  Neither ever
+// changes a result; they exist to reproduce the measurements behind the
+// defaults.  Each is read once per process.
+int64_t fused_run_elems_override() {
+  static const int64_t v = env_count("DASO_FUSED_RUN_ELEMS", -1, int64_t(1) << 30);
   return v;
+}
+int64_t fused_cap_override() {
+  static const int64_t v = env_count("DASO_FUSED_WG_PER_CU", -1, 64);
+  return v;
+}
+
+// Streams a launch touches (the tile-order and occupancy rules go by it).
+int launch_streams(daso::Mode mode, const StepArgs& a) {
+  if (mode == daso::kModeAvg) return a.g + 1;
+  if (mode == daso::kModeMerge) return a.P + 2 + (a.wire ? 1 : 0);
+  if (mode == daso::kModeFused) return a.g + a.P + 4 + (a.wire ? 1 : 0) + (a.gavg ? 1 : 0);
+  return 2;
+}
+
+// Tiles per XCD run of one launch of `ntiles` tiles of `tile` elements (the
+// rule and its measurements are stated with the constants in daso_launch.h).
+int32_t xcd_run_of(daso::Mode mode, int streams, int64_t ntiles, int64_t tile) {
+  if (mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams) {
+    const int64_t over = fused_run_elems_override();
+    if (over >= 0) return static_cast<int32_t>(std::max<int64_t>(1, over / tile));
+    int64_t run = 1;
+    while (run * 2 <= ntiles / (8 * daso::kXcdRunBlocksPerLaunch) && run < (int64_t(1) << 20)) run *= 2;
+    return static_cast<int32_t>(run);
+  }
+  if (streams >= daso::kXcdRunManyStreams) return daso::kXcdRunMany;
+  if (streams >= daso::kXcdRunMidStreams) return daso::kXcdRunMid;
+  return 1;
+}
+
+// LDS per workgroup of a launch: the occupancy cap of the fused step.
+int32_t lds_of(daso::Mode mode, int streams) {
+  if (mode != daso::kModeFused) return 0;
+  const int64_t over = fused_cap_override();
+  if (over >= 0) return daso::lds_for_workgroups_per_cu(static_cast<int32_t>(over));
+  return streams >= daso::kCapStreams ? daso::lds_for_workgroups_per_cu(daso::kCapWorkgroupsPerCU) : 0;
 }
 
 // The current device, which must also be the device of `stream` (kernels run
@@ -176,17 +216,8 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   int dev = 0;
   const int drc = current_device(stream, &dev);
   if (drc != DASO_OK) return drc;
-  // tile order across the XCDs, by the number of streams the launch touches
-  // (the measured rule is stated with the constants in daso_launch.h)
-  int streams = 2;
-  if (mode == daso::kModeAvg) streams = a.g + 1;
-  if (mode == daso::kModeMerge) streams = a.P + 2 + (a.wire ? 1 : 0);
-  if (mode == daso::kModeFused) streams = a.g + a.P + 4 + (a.wire ? 1 : 0) + (a.gavg ? 1 : 0);
-  a.xcd_run = 1;
-  if (streams >= daso::kXcdRunManyStreams) a.xcd_run = daso::kXcdRunMany;
-  else if (streams >= daso::kXcdRunMidStreams) a.xcd_run = daso::kXcdRunMid;
-  else if (mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams)
-    a.xcd_run = static_cast<int32_t>(std::max<int64_t>(1, fused_run_elems() / tile));
+  const int streams = launch_streams(mode, a);
+  const int32_t lds = lds_of(mode, streams);
   std::unique_lock<std::mutex> hold;
   if (with_stats) {
     void* base = nullptr;
@@ -209,8 +240,10 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   for (const auto& gr : groups) {
     fill_group(a, b, gr, tile);
     a.stats = with_stats ? stats + gr.first : nullptr;
+    a.xcd_run = xcd_run_of(mode, streams, a.ntiles, tile);
     const int64_t grid = daso::host::launch_grid(a.ntiles, a.xcd_run);
-    if (daso::launch_step(mode, with_stats, a, static_cast<uint32_t>(grid), stream) != hipSuccess)
+    if (daso::launch_step(mode, with_stats, a, static_cast<uint32_t>(grid), static_cast<uint32_t>(lds), stream) !=
+        hipSuccess)
       return DASO_EHIP;
   }
   return DASO_OK;
@@ -280,14 +313,20 @@ int daso_global_merge_f32(float* params, const float* const* stale, int32_t P, c
 
 namespace {
 
-int fused_impl(const daso_sync_args* args, hipStream_t stream, Space space) {
+// Checks a fused call and fills the kernel arguments that do not depend on the
+// launch (streams, counts, constants).  With n == 0 only the counts and the
+// exchange type are filled: no pointer is looked at.
+int fused_args(const daso_sync_args* args, StepArgs& a) {
   if (args == nullptr) return DASO_EINVAL;
   const daso_sync_args& s = *args;
   daso::host::FusedView v;
   const int rc = daso::host::check_fused(s, &v);
-  if (rc != DASO_OK || s.n == 0) return rc;
-  StepArgs a;
+  if (rc != DASO_OK) return rc;
   memset(&a, 0, sizeof(a));
+  a.g = s.g;
+  a.P = s.P;
+  a.xf32 = (s.flags & DASO_EXCHANGE_F32) ? 1 : 0;
+  if (s.n == 0) return DASO_OK;
   for (int32_t r = 0; r < s.g; ++r) a.grads[r] = s.grads[r];
   for (int32_t i = 0; i < s.P; ++i) a.stale[i] = v.stale[i];
   a.g = s.g;
@@ -300,8 +339,14 @@ int fused_impl(const daso_sync_args* args, hipStream_t stream, Space space) {
   a.mu = s.mu;
   a.wd = s.weight_decay;
   a.flags = s.flags;
-  a.xf32 = v.xf32 ? 1 : 0;
-  return run_groups(daso::kModeFused, a, s.buckets, s.nbuckets, s.stats, stream, space);
+  return DASO_OK;
+}
+
+int fused_impl(const daso_sync_args* args, hipStream_t stream, Space space) {
+  StepArgs a;
+  const int rc = fused_args(args, a);
+  if (rc != DASO_OK || args->n == 0) return rc;
+  return run_groups(daso::kModeFused, a, args->buckets, args->nbuckets, args->stats, stream, space);
 }
 
 }  // namespace
@@ -314,6 +359,25 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream) {
 
 int daso_fused_sync_step_noalloc(const daso_sync_args* args, hipStream_t stream) {
   return fused_impl(args, stream, Space::kFixed);
+}
+
+int daso_fused_launch_config(const daso_sync_args* args, daso_launch_config* out) {
+  if (out == nullptr) return DASO_EINVAL;
+  StepArgs a;
+  const int rc = fused_args(args, a);
+  if (rc != DASO_OK) return rc;
+  const bool with_stats = args->stats != nullptr;
+  const int64_t tile = daso::tile_elems(daso::kModeFused, with_stats, a);
+  const int streams = launch_streams(daso::kModeFused, a);
+  int64_t ntiles = 0;
+  if (args->n > 0)
+    for (int32_t k = 0; k < std::min<int32_t>(args->nbuckets, daso::kLaunchBuckets); ++k)
+      ntiles += daso::tiles_of(args->buckets[k].start, args->buckets[k].start + args->buckets[k].numel, tile);
+  out->tile_elems = tile;
+  out->ntiles = ntiles;
+  out->xcd_run_tiles = xcd_run_of(daso::kModeFused, streams, std::max<int64_t>(ntiles, 1), tile);
+  out->lds_bytes = lds_of(daso::kModeFused, streams);
+  return DASO_OK;
 }
 
 }  // extern "C"

@@ -89,10 +89,10 @@ __global__ __launch_bounds__(kProbeBlock) void probe_kernel(const ProbeArgs a) {
 }
 
 template <int R32, int R16, int W32, int W16, int ITERS>
-hipError_t launch(const ProbeArgs& a, uint32_t grid, hipStream_t stream) {
+hipError_t launch(const ProbeArgs& a, uint32_t grid, uint32_t lds, hipStream_t stream) {
   void* args[] = {const_cast<ProbeArgs*>(&a)};
   return hipLaunchKernel(reinterpret_cast<const void*>(&probe_kernel<R32, R16, W32, W16, ITERS>), dim3(grid),
-                         dim3(kProbeBlock), args, 0, stream);
+                         dim3(kProbeBlock), args, lds, stream);
 }
 
 // The access shapes of the fused step on the five workloads (g + 2 fp32 reads,
@@ -113,13 +113,15 @@ extern "C" {
 
 // Runs one probe: r32/r16 read streams and w32/w16 written streams (host arrays
 // of device pointers, each stream at least n elements of 4 or 2 bytes), tiles of
-// 1024 * iters elements in runs of xcd_run tiles per XCD.  Returns 0, -1 for a
-// shape without an instance or invalid sizes/pointers, -4 when the launch
-// fails.  Nothing is launched on -1.
+// 1024 * iters elements in runs of xcd_run tiles per XCD, each workgroup holding
+// lds_bytes of (unused) LDS, which caps how many share a CU, as the step's
+// launches do.  Returns 0, -1 for a shape without an instance or invalid
+// sizes/pointers, -4 when the launch fails.  Nothing is launched on -1.
 int daso_probe_run(const void* const* rd32, int32_t r32, const void* const* rd16, int32_t r16, void* const* wr32,
                    int32_t w32, void* const* wr16, int32_t w16, uint32_t* sink, int64_t n, int32_t iters,
-                   int32_t xcd_run, hipStream_t stream) {
+                   int32_t xcd_run, int32_t lds_bytes, hipStream_t stream) {
   if (n <= 0 || n % 4 != 0 || (iters != 1 && iters != 2) || xcd_run < 1 || sink == nullptr) return -1;
+  if (lds_bytes < 0 || lds_bytes > 160 * 1024) return -1;
   if (r32 < 0 || r32 > kMaxRead || r16 < 0 || r16 > kMaxRead || w32 < 0 || w32 > kMaxWrite || w16 < 0 ||
       w16 > kMaxWrite)
     return -1;
@@ -151,9 +153,10 @@ int daso_probe_run(const void* const* rd32, int32_t r32, const void* const* rd16
   const int64_t block = 8 * int64_t(xcd_run);
   const int64_t cap = int64_t(1) << 20;
   const int64_t grid = ntiles <= cap ? ntiles : (block <= cap ? (cap / block) * block : cap);
-#define DASO_PROBE_CASE(A, B, C, D, E)                                                     \
-  if (r32 == (A) && r16 == (B) && w32 == (C) && w16 == (D) && iters == (E))                \
-    return launch<A, B, C, D, E>(a, static_cast<uint32_t>(grid), stream) == hipSuccess ? 0 : -4;
+  const uint32_t g32 = static_cast<uint32_t>(grid), lds = static_cast<uint32_t>(lds_bytes);
+#define DASO_PROBE_CASE(A, B, C, D, E)                                      \
+  if (r32 == (A) && r16 == (B) && w32 == (C) && w16 == (D) && iters == (E)) \
+    return launch<A, B, C, D, E>(a, g32, lds, stream) == hipSuccess ? 0 : -4;
   DASO_PROBE_SHAPES(DASO_PROBE_CASE)
 #undef DASO_PROBE_CASE
   return -1;

@@ -162,7 +162,7 @@ int64_t launch_grid(int64_t ntiles, int32_t run) {
 
 extern "C" {
 
-int daso_abi_version(void) { return 101; }
+int daso_abi_version(void) { return 102; }
 
 int32_t daso_plan_buckets(const int64_t* numels, int32_t ntensors, int64_t cap_elems, const int32_t* S_cycle,
                           int32_t n_cycle, daso_bucket* out, int32_t out_cap) {

@@ -437,13 +437,16 @@ __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64
         if (e0 + k >= tlo && e0 + k < thi) mask |= 1u << k;
     }
     if constexpr (kBatched) {
-      VecIn<MODE, G, PP, XF> v;
       if (full) {
+        VecIn<MODE, G, PP, XF> v;
         load_in<MODE, G, PP, XF, true>(a, e0, mask, v);
         finish<MODE, G, PP, XF, true, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
       } else {
-        load_in<MODE, G, PP, XF, false>(a, e0, mask, v);
-        finish<MODE, G, PP, XF, false, STATS>(a, e0, mask, v, two_s, qg, qm, acc);
+        // A vector cut by the bucket edge takes its elements one by one; folding
+        // each stream in as it loads keeps this rarely run path from holding
+        // every stream's addresses and values at once, which would otherwise set
+        // the register count, and so the occupancy, of the whole kernel.
+        step_vec<MODE, G, PP, false, STATS, XF>(a, e0, mask, two_s, qg, qm, acc);
       }
     } else {
       if (full) step_vec<MODE, G, PP, true, STATS, XF>(a, e0, mask, two_s, qg, qm, acc);
@@ -648,12 +651,13 @@ auto dispatch(Mode mode, bool with_stats, const StepArgs& a, const F& f) {
 struct Launcher {
   const StepArgs& a;
   uint32_t grid;
+  uint32_t lds;  // LDS held per workgroup (unused by the kernel; caps workgroups per CU)
   hipStream_t stream;
   template <int MODE, int G, int PP, bool STATS, bool XF>
   hipError_t run() const {
     void* args[] = {const_cast<StepArgs*>(&a)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&step_kernel<MODE, G, PP, STATS, XF>),
-                                         dim3(grid), dim3(kBlock), args, 0, stream);
+                                         dim3(grid), dim3(kBlock), args, lds, stream);
     if (e != hipSuccess || !STATS) return e;
     StatsArgs sa = {a.partials, a.tile_table, a.stats, a.nb};
     void* sargs[] = {&sa};
@@ -674,8 +678,9 @@ int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& a) {
   return dispatch(mode, with_stats, a, TileSize{});
 }
 
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, uint32_t grid, hipStream_t stream) {
-  return dispatch(mode, with_stats, a, Launcher{a, grid, stream});
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, uint32_t grid, uint32_t lds,
+                       hipStream_t stream) {
+  return dispatch(mode, with_stats, a, Launcher{a, grid, lds, stream});
 }
 
 }  // namespace daso

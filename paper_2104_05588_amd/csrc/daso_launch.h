@@ -32,20 +32,43 @@ constexpr bool kNtParams = DASO_NT_PARAMS != 0;  // non-temporal access to param
 constexpr int kGenericIters = 2;                 // vectors per thread for runtime stream counts
 constexpr int kLaunchBuckets = 64;
 // Tile order across the 8 XCDs: workgroups go to the XCDs in turn, and a
-// launch runs faster when each XCD takes runs of consecutive tiles.  Measured
-// against plain order on several MI355X: runs of 32 tiles +4 to 5% with 45
-// streams; runs of 16 between -2.3% and +5.5% with 25 (three boxes).  Below 20
-// streams the fused step is fastest with runs of 32K elements, 128 KB of each
-// fp32 stream (16 tiles of 2048 elements, 32 of 1024): the resnet50-shaped
-// step +0.3 to +2.7% on six boxes; fp32 exchange with 1024-element tiles +1
-// to +8%.  The separate entry points move by about 1% either way and keep
-// plain order there.
-constexpr int kXcdRunFusedStreams = 9;        // fused step: runs of kXcdRunFusedElems from here
-constexpr int64_t kXcdRunFusedElems = 32768;  // elements per run (a multiple of every tile)
-constexpr int kXcdRunMidStreams = 20;   // any launch: runs of kXcdRunMid tiles from here
+// launch runs faster when each XCD takes runs of consecutive tiles.
+//  - Fused step from 9 streams: runs of ntiles / 512 tiles rounded down to a
+//    power of two (about 64 blocks of 8 runs per launch): 16 tiles of 2048
+//    elements for the resnet50-shaped step, 128 of 1024 for the
+//    segmentation-shaped one, 512 of 1024 for the GPT-shaped one.  Measured on
+//    MI355X against the runs that were best for a fixed stream count: the
+//    GPT-shaped step 2 to 3% faster with 256 to 512 tiles than with 32 (two
+//    boxes), the same 45 streams over the 25.6M-parameter set best at 16 to 32,
+//    the resnet50-shaped step best at 32K elements, the segmentation-shaped one
+//    at 128K to 512K or plain order under the occupancy cap below.
+//  - Other launches: runs of 32 tiles from 32 streams, 16 from 20 (+4 to 5%
+//    with 45 streams, -2.3 to +5.5% with 25), plain order below (the separate
+//    entry points move by about 1% either way).
+constexpr int kXcdRunFusedStreams = 9;         // fused step: runs scaled to the launch from here
+constexpr int64_t kXcdRunBlocksPerLaunch = 64;  // fused step: about this many blocks of 8 runs
+constexpr int kXcdRunMidStreams = 20;   // other launches: runs of kXcdRunMid tiles from here
 constexpr int kXcdRunMid = 16;
-constexpr int kXcdRunManyStreams = 32;  // any launch: runs of kXcdRunMany tiles from here
+constexpr int kXcdRunManyStreams = 32;  // other launches: runs of kXcdRunMany tiles from here
 constexpr int kXcdRunMany = 32;
+
+// Occupancy of the fused step.  Loads of a workgroup's whole tile are in flight
+// at once, and the step runs faster with fewer of them: a fused launch of at
+// least kCapStreams streams holds enough LDS per workgroup (the kernel uses none
+// of it) that at most kCapWorkgroupsPerCU share a CU, i.e. 2 waves per SIMD.
+// Measured on four MI355X boxes: the resnet50-shaped step 2.5 to 5% faster
+// (212.9 against 223.6 us cold on one), the segmentation-shaped one 2.6 to 4%,
+// the node shapes from g = 4, P = 2 up 1 to 5%; 3 per CU gains at most 1%, 1
+// per CU loses 10%.  Launches of fewer streams keep their occupancy (the local
+// step g = 4, P = 0 with 9 streams is 1% slower capped; the pack with 2 is 40%
+// slower), as do the separate entry points.
+constexpr int kCapStreams = 10;
+constexpr int kCapWorkgroupsPerCU = 2;
+constexpr int32_t kCuLdsBytes = 160 * 1024;  // LDS per CU on gfx950
+
+// LDS per workgroup that lets at most k workgroups share a CU: a 1 KB margin
+// covers the kernel's own few bytes of LDS and the allocation granule.
+inline int32_t lds_for_workgroups_per_cu(int32_t k) { return k >= 1 ? kCuLdsBytes / k - 1024 : 0; }
 
 enum Mode : int { kModeAvg = 0, kModePack = 1, kModeMerge = 2, kModeFused = 3 };
 
@@ -124,8 +147,9 @@ inline int64_t tiles_of(int64_t start, int64_t end, int64_t tile) {
 int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& args);
 
 // Enqueue one launch of `mode` over the buckets in `args` (args.ntiles tiles,
-// counted with tile_elems()) on `grid` workgroups: one per tile, or fewer, each
-// then looping over tiles grid apart.
-hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, uint32_t grid, hipStream_t stream);
+// counted with tile_elems()) on `grid` workgroups (one per tile, or fewer, each
+// then looping over tiles grid apart), each holding `lds` bytes of LDS.
+hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, uint32_t grid, uint32_t lds,
+                       hipStream_t stream);
 
 }  // namespace daso

@@ -45,7 +45,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_status_strings_and_version(lib):
-    assert lib.daso_abi_version() == 101
+    assert lib.daso_abi_version() == 102
     for code in (L.DASO_OK, L.DASO_EINVAL, L.DASO_EALIGN, L.DASO_EALIAS, L.DASO_EHIP, L.DASO_ENOSPACE):
         s = L.status_string(code)
         assert s.startswith("DASO_")
@@ -60,7 +60,8 @@ def test_struct_layouts_match_header(tmp_path):
               "daso_bucket_stats": [f[0] for f in L.daso_bucket_stats._fields_],
               "daso_sync_args": [f[0] for f in L.daso_sync_args._fields_],
               "daso_schedule_config": [f[0] for f in L.daso_schedule_config._fields_],
-              "daso_batch_plan": [f[0] for f in L.daso_batch_plan._fields_]}
+              "daso_batch_plan": [f[0] for f in L.daso_batch_plan._fields_],
+              "daso_launch_config": [f[0] for f in L.daso_launch_config._fields_]}
     src = ["#include <stdio.h>", "#include <stddef.h>", '#include "daso.h"', "int main(void) {"]
     for st, names in fields.items():
         src.append(f'  printf("{st} size %zu\\n", sizeof({st}));')
@@ -387,3 +388,96 @@ def test_plan_buckets_random_and_edges(lib):
     assert f((ctypes.c_int64 * 1)(4), 1, 0, one, 1, None, 0) == L.DASO_EINVAL
     assert f((ctypes.c_int64 * 1)(4), 1, 10, (ctypes.c_int32 * 1)(-2), 1, None, 0) == L.DASO_EINVAL
     assert f((ctypes.c_int64 * 1)(4), 1, 10, one, 1, None, 1) == L.DASO_EINVAL
+
+
+# ----------------------------------------------------------- launch shape
+def _tiles_of(start, end, tile):
+    return 0 if end <= start else (end - 1) // tile - start // tile + 1
+
+
+def _shape_args(n, g, P, buckets, wire=True, stats=True, f32=False):
+    """Fake, disjoint 2 GiB-spaced buffers (never dereferenced) for a fused call."""
+    GB2 = 2 << 30
+    a = L.daso_sync_args()
+    keep = [ptrs(*[A + r * GB2 for r in range(g)]), ptrs(*[A + (g + i) * GB2 for i in range(P)]),
+            L.bucket_table(buckets)]
+    a.n, a.g, a.P = n, g, P
+    a.grads = keep[0]
+    if f32:
+        a.stale_f32, a.flags = keep[1], L.DASO_EXCHANGE_F32
+    else:
+        a.stale = keep[1]
+    a.params, a.momentum = A + (g + P) * GB2, A + (g + P + 1) * GB2
+    w = A + (g + P + 2) * GB2 if wire else None
+    if f32:
+        a.wire_f32 = w
+    else:
+        a.wire = w
+    a.stats = A + (g + P + 3) * GB2 if stats else None
+    a.buckets, a.nbuckets = keep[2], len(buckets)
+    a.lr, a.mu = 0.1, 0.9
+    return a, keep
+
+
+def _config(lib, a):
+    c = L.daso_launch_config()
+    rc = lib.daso_fused_launch_config(ctypes.byref(a), ctypes.byref(c))
+    return rc, {f: getattr(c, f) for f, _ in L.daso_launch_config._fields_}
+
+
+def test_fused_launch_config_follows_the_stated_rule(lib):
+    """daso_fused_launch_config against the rule in daso.h, written out here:
+    tiles of 2048 elements when a vector's inputs fit in 48 registers (4g + 2P
+    + 8 for bf16 copies, 4g + 4P + 8 for fp32), else 1024; from 9 streams, runs
+    of ntiles / 512 tiles rounded down to a power of two; from 10 streams, LDS
+    that lets 2 workgroups share a 160 KB CU."""
+    from workloads import recipes as R
+    cap_lds = 160 * 1024 // 2 - 1024
+    cases = []
+    for name in ("resnet50", "gpt_medium", "segnet", "resnet18"):
+        w = R.workload(name)
+        cases.append((w.n, w.g, w.P, [(b.start, b.numel, b.S) for b in w.buckets], True, False))
+    cases += [(25_557_032, 4, 0, [(0, 25_557_032, 1)], True, False),     # 9 streams
+              (1_000_000, 1, 0, [(0, 1_000_000, 1)], False, False),     # 5 streams
+              (25_557_032, 4, 8, [(0, 25_557_032, 2)], True, True)]     # fp32 exchange
+    for n, g, P, bks, wire, f32 in cases:
+        a, keep = _shape_args(n, g, P, bks, wire=wire, f32=f32)
+        rc, c = _config(lib, a)
+        assert rc == L.DASO_OK
+        regs = 4 * g + (4 if f32 else 2) * P + 8
+        tile = 2048 if regs <= 48 else 1024
+        ntiles = sum(_tiles_of(s, s + k, tile) for (s, k, _) in bks[:64])
+        streams = g + P + 4 + (1 if wire else 0)
+        run = 1
+        if streams >= 9:
+            while run * 2 <= ntiles // 512:
+                run *= 2
+        want = {"tile_elems": tile, "ntiles": ntiles, "xcd_run_tiles": run,
+                "lds_bytes": cap_lds if streams >= 10 else 0}
+        assert c == want, (n, g, P, c, want)
+    w = R.workload("resnet50")
+    a, keep = _shape_args(w.n, w.g, w.P, [(b.start, b.numel, b.S) for b in w.buckets])
+    assert _config(lib, a)[1]["xcd_run_tiles"] == 16 and _config(lib, a)[1]["tile_elems"] == 2048
+    a.momentum = a.params + 64                      # rejected as the step rejects it
+    assert _config(lib, a)[0] == L.DASO_EALIAS
+    assert lib.daso_fused_launch_config(ctypes.byref(a), None) == L.DASO_EINVAL
+
+
+def test_fused_launch_config_overrides(tmp_path):
+    """DASO_FUSED_RUN_ELEMS and DASO_FUSED_WG_PER_CU replace the run length and
+    the occupancy cap (read once per process, so in a child process)."""
+    import json
+    import subprocess
+    import sys
+    code = (
+        "import ctypes, json, sys; sys.path.insert(0, %r); from tests import test_abi_host as T; "
+        "from paper_2104_05588_amd import _lib as L; lib = L.load(); "
+        "a, k = T._shape_args(25_557_032, 4, 8, [(0, 25_557_032, 4)]); print(json.dumps(T._config(lib, a)[1]))"
+        % ROOT)
+    for env, want in (({"DASO_FUSED_RUN_ELEMS": "0", "DASO_FUSED_WG_PER_CU": "0"}, (1, 0)),
+                      ({"DASO_FUSED_RUN_ELEMS": "131072", "DASO_FUSED_WG_PER_CU": "3"}, (64, 160 * 1024 // 3 - 1024)),
+                      ({"DASO_FUSED_RUN_ELEMS": "junk"}, (16, 160 * 1024 // 2 - 1024))):
+        out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, check=True,
+                             env=dict(os.environ, **env), cwd=ROOT).stdout
+        c = json.loads(out.strip().splitlines()[-1])
+        assert (c["xcd_run_tiles"], c["lds_bytes"]) == want, (env, c)

@@ -872,7 +872,7 @@ import torch
 sys.path.insert(0, sys.argv[1])
 import paper_2104_05588_amd as daso
 torch.cuda.set_device(0)
-n, g, P = 1_200_007, 4, 8
+n, g, P = 1_200_007, int(sys.argv[2]), int(sys.argv[3])
 bks = [(0, 500_003, 4), (500_003, n - 500_003, 2)]
 gen = torch.Generator(device="cuda")
 gen.manual_seed(77)
@@ -891,22 +891,25 @@ sys.stdout.buffer.write(out.tobytes())
 """
 
 
-def test_tile_order_never_changes_a_result():
-    """DASO_FUSED_RUN_ELEMS changes only which XCD takes which tiles: plain
-    order, the default runs and longer or shorter runs give the same bits."""
+@pytest.mark.parametrize("g,P", [(4, 8), (8, 32)])
+def test_launch_shape_never_changes_a_result(g, P):
+    """DASO_FUSED_RUN_ELEMS and DASO_FUSED_WG_PER_CU change only which XCD takes
+    which tiles and how many workgroups share a CU: plain order, the default
+    runs, longer or shorter runs, no occupancy cap and caps of 1 to 3 workgroups
+    per CU all give the same bits (2048- and 1024-element tiles)."""
     import os
     import subprocess
     import sys
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     outs = {}
-    for v in ("", "0", "4096", "65536", "1048576"):
-        announce("tile order, DASO_FUSED_RUN_ELEMS =", repr(v))
-        env = dict(os.environ, DASO_FUSED_RUN_ELEMS=v)
-        res = subprocess.run([sys.executable, "-c", _RUN_ORDER_SCRIPT, root], capture_output=True, env=env,
-                             timeout=110)
+    for run, cap in (("", ""), ("0", "0"), ("4096", "1"), ("65536", "3"), ("1048576", "2")):
+        announce("launch shape g=", g, "P=", P, "DASO_FUSED_RUN_ELEMS =", repr(run), "DASO_FUSED_WG_PER_CU =", repr(cap))
+        env = dict(os.environ, DASO_FUSED_RUN_ELEMS=run, DASO_FUSED_WG_PER_CU=cap)
+        res = subprocess.run([sys.executable, "-c", _RUN_ORDER_SCRIPT, root, str(g), str(P)], capture_output=True,
+                             env=env, timeout=110)
         assert res.returncode == 0, res.stderr.decode()[-2000:]
-        outs[v] = res.stdout
-    base = outs[""]
+        outs[(run, cap)] = res.stdout
+    base = outs[("", "")]
     assert len(base) > 0
     for v, o in outs.items():
         assert o == base, v
