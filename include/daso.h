@@ -63,10 +63,17 @@
  *  - Launch shape: the fused step hands each XCD runs of consecutive tiles
  *    (about 64 blocks of 8 runs per launch from 9 streams) and, from 10
  *    streams, lets at most 2 workgroups share a CU; both were measured best on
- *    MI355X (daso_fused_launch_config reports them).  The environment variables
- *    DASO_FUSED_RUN_ELEMS (elements per run, 0 = plain order) and
- *    DASO_FUSED_WG_PER_CU (0 = no cap), read once per process, replace them to
- *    reproduce the measurements.  Neither ever changes a result.
+ *    MI355X (daso_fused_launch_config reports them).  For each shape of a
+ *    single launch (up to 64 buckets), the first 4 calls of
+ *    daso_fused_sync_step alternate between those runs and plain tile order,
+ *    timed with events on the call's stream that later calls poll (never wait
+ *    on); once they have completed, the faster order is kept for the shape.
+ *    Captured calls take no samples, and polling is skipped while a HIP error
+ *    is pending on the calling thread, so that error stays for the caller.
+ *    The environment variables DASO_FUSED_RUN_ELEMS (elements per run, 0 =
+ *    plain order; no sampling), DASO_FUSED_WG_PER_CU (0 = no cap) and
+ *    DASO_FUSED_TUNE (0 = no sampling), read once per process, replace them to
+ *    reproduce the measurements.  None of this ever changes a result.
  *  - Calls may be made from several host threads.  Fused steps with statistics
  *    share one small per-(device, stream) workspace (24 bytes per tile of 1024
  *    or 2048 parameters, plus a 260-byte table of bucket ranges) that the
@@ -225,8 +232,10 @@ int daso_fused_sync_step_noalloc(const daso_sync_args* args, hipStream_t stream)
  * xcd_run_tiles consecutive tiles (1: plain order), and give each workgroup
  * lds_bytes of LDS (unused by the kernel; it caps how many workgroups share a
  * CU; 0: no cap).  ntiles counts the tiles of the first launch (the first 64
- * buckets).  The arguments are checked as the step checks them and the same
- * status is returned; *out is written only on DASO_OK. */
+ * buckets).  Once the tile order of the shape has been chosen from its first
+ * calls on the current device, xcd_run_tiles reports that choice.  The
+ * arguments are checked as the step checks them and the same status is
+ * returned; *out is written only on DASO_OK. */
 typedef struct daso_launch_config {
   int64_t tile_elems;
   int64_t ntiles;

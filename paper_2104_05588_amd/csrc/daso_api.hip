@@ -193,6 +193,115 @@ int current_device(hipStream_t stream, int* dev) {
   return sdev == *dev ? DASO_OK : DASO_EINVAL;
 }
 
+// ----------------------------------------------------------- tile-order choice
+// The rule's run length is the best measured for most fused shapes, but some
+// (the segmentation-shaped step) run 2 to 5% faster in plain order.  For each
+// fused launch shape of a single launch, the first kTuneSamples calls alternate
+// between the rule's run length and plain order, each bracketed by two events
+// on the call's stream.  Once the last of them has completed, which later calls
+// poll with hipEventQuery (never waiting), the order with the shorter fastest
+// sample is kept for the shape; until then calls take the rule's run length.
+// The order never changes a result.  No sample is taken by a captured call, by
+// daso_fused_sync_step_noalloc (it only reads a choice already made), or when
+// DASO_FUSED_RUN_ELEMS or DASO_FUSED_TUNE=0 is set.
+constexpr int kTuneSamples = 4;  // rule, plain, rule, plain
+
+bool tuning_enabled() {
+  static const bool v = env_count("DASO_FUSED_TUNE", 1, 1) != 0 && fused_run_elems_override() < 0;
+  return v;
+}
+
+struct TuneKey {
+  int dev;
+  int32_t g, P, xf32, stats, outputs;
+  int64_t n;
+  uint64_t layout;  // hash of the bucket table
+  bool operator<(const TuneKey& o) const {
+    if (dev != o.dev) return dev < o.dev;
+    if (g != o.g) return g < o.g;
+    if (P != o.P) return P < o.P;
+    if (xf32 != o.xf32) return xf32 < o.xf32;
+    if (stats != o.stats) return stats < o.stats;
+    if (outputs != o.outputs) return outputs < o.outputs;
+    if (n != o.n) return n < o.n;
+    return layout < o.layout;
+  }
+};
+
+struct Tune {
+  std::mutex mu;
+  hipEvent_t ev[kTuneSamples][2] = {};
+  int taken = 0;       // samples whose launches are queued
+  int32_t chosen = 0;  // tiles per run once decided, 0 before
+  bool off = false;    // an event call failed: keep the rule for this shape
+};
+
+std::mutex g_tune_mu;  // guards the map itself; nodes never move or go away
+std::map<TuneKey, Tune> g_tune;
+
+uint64_t layout_hash(const daso_bucket* b, int32_t nb) {
+  uint64_t h = 1469598103934665603ull;  // FNV-1a over the bucket ranges
+  auto mix = [&h](uint64_t v) {
+    for (int k = 0; k < 8; ++k) {
+      h ^= (v >> (8 * k)) & 0xFFu;
+      h *= 1099511628211ull;
+    }
+  };
+  for (int32_t i = 0; i < nb; ++i) {
+    mix(static_cast<uint64_t>(b[i].start));
+    mix(static_cast<uint64_t>(b[i].numel));
+  }
+  return h;
+}
+
+TuneKey tune_key(int dev, const StepArgs& a, bool with_stats, const daso_bucket* b, int32_t nb) {
+  int64_t n = 0;  // the buckets tile [0, n)
+  for (int32_t i = 0; i < nb; ++i) n += b[i].numel;
+  return TuneKey{dev, a.g, a.P, a.xf32, with_stats ? 1 : 0, (a.wire ? 1 : 0) | (a.gavg ? 2 : 0), n,
+                 layout_hash(b, nb)};
+}
+
+// The decided run length of a shape, or 0.  Never inserts.
+int32_t tuned_run(const TuneKey& k) {
+  std::lock_guard<std::mutex> lock(g_tune_mu);
+  const auto it = g_tune.find(k);
+  if (it == g_tune.end()) return 0;
+  std::lock_guard<std::mutex> tl(it->second.mu);
+  return it->second.chosen;
+}
+
+Tune& tune_entry(const TuneKey& k) {
+  std::lock_guard<std::mutex> lock(g_tune_mu);
+  return g_tune[k];
+}
+
+// With t.mu held, after all samples were queued: decide once the last has
+// completed.  The query runs only when no error is pending on this thread, and
+// the not-ready status it may leave is cleared, so a caller's error is neither
+// consumed nor masked.
+void try_decide(Tune& t, int32_t rule) {
+  if (hipPeekAtLastError() != hipSuccess) return;
+  const hipError_t q = hipEventQuery(t.ev[kTuneSamples - 1][1]);
+  if (q != hipSuccess) {
+    if (hipPeekAtLastError() != hipSuccess) (void)hipGetLastError();
+    if (q != hipErrorNotReady) t.off = true;
+    return;
+  }
+  float best[2] = {1e30f, 1e30f};
+  for (int k = 0; k < kTuneSamples; ++k) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, t.ev[k][0], t.ev[k][1]) != hipSuccess) {
+      t.off = true;
+      return;
+    }
+    best[k % 2] = std::min(best[k % 2], ms);
+  }
+  t.chosen = best[1] < best[0] ? 1 : rule;
+  for (auto& e : t.ev)
+    for (hipEvent_t& x : e)
+      if (x) (void)hipEventDestroy(x), x = nullptr;
+}
+
 // Where a fused launch with statistics keeps its tile partials and table.
 enum class Space {
   kAllocated,  // the per-(device, stream) workspace, allocated on first use
@@ -237,14 +346,60 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     a.partials = static_cast<TilePartial*>(base);
     a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(base) + table_at);
   }
+  // the tile order of a single fused launch may be chosen per shape (above)
+  const bool choosable = mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams && groups.size() == 1 &&
+                         tuning_enabled();
   for (const auto& gr : groups) {
     fill_group(a, b, gr, tile);
     a.stats = with_stats ? stats + gr.first : nullptr;
-    a.xcd_run = xcd_run_of(mode, streams, a.ntiles, tile);
+    const int32_t rule = xcd_run_of(mode, streams, a.ntiles, tile);
+    a.xcd_run = rule;
+    Tune* t = nullptr;
+    std::unique_lock<std::mutex> tl;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (choosable) {
+      const TuneKey key = tune_key(dev, a, with_stats, b, nb);
+      if (space == Space::kFixed) {
+        const int32_t c = tuned_run(key);
+        if (c > 0) a.xcd_run = c;
+      } else {
+        t = &tune_entry(key);
+        tl = std::unique_lock<std::mutex>(t->mu);
+        if (t->chosen > 0) {
+          a.xcd_run = t->chosen;
+        } else if (!t->off && t->taken < kTuneSamples) {
+          hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+          if (hipStreamIsCapturing(stream, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
+            hipEvent_t(&ev)[2] = t->ev[t->taken];
+            if ((ev[0] || hipEventCreate(&ev[0]) == hipSuccess) && (ev[1] || hipEventCreate(&ev[1]) == hipSuccess)) {
+              e0 = ev[0];
+              e1 = ev[1];
+              a.xcd_run = (t->taken % 2 == 0) ? rule : 1;
+            } else {
+              t->off = true;
+            }
+          }
+        } else if (!t->off && t->taken == kTuneSamples) {
+          try_decide(*t, rule);
+          if (t->chosen > 0) a.xcd_run = t->chosen;
+        }
+      }
+    }
     const int64_t grid = daso::host::launch_grid(a.ntiles, a.xcd_run);
+    if (e0 && hipEventRecord(e0, stream) != hipSuccess) {
+      t->off = true;
+      e1 = nullptr;
+    }
     if (daso::launch_step(mode, with_stats, a, static_cast<uint32_t>(grid), static_cast<uint32_t>(lds), stream) !=
         hipSuccess)
       return DASO_EHIP;
+    if (e1) {
+      if (hipEventRecord(e1, stream) == hipSuccess) {
+        ++t->taken;
+      } else {
+        t->off = true;
+      }
+    }
   }
   return DASO_OK;
 }
@@ -377,6 +532,13 @@ int daso_fused_launch_config(const daso_sync_args* args, daso_launch_config* out
   out->ntiles = ntiles;
   out->xcd_run_tiles = xcd_run_of(daso::kModeFused, streams, std::max<int64_t>(ntiles, 1), tile);
   out->lds_bytes = lds_of(daso::kModeFused, streams);
+  // a tile order already chosen for this shape on the current device replaces the rule's
+  int dev = 0;
+  if (args->n > 0 && streams >= daso::kXcdRunFusedStreams && args->nbuckets <= daso::kLaunchBuckets &&
+      tuning_enabled() && hipGetDevice(&dev) == hipSuccess) {
+    const int32_t c = tuned_run(tune_key(dev, a, with_stats, args->buckets, args->nbuckets));
+    if (c > 0) out->xcd_run_tiles = c;
+  }
   return DASO_OK;
 }
 

@@ -802,6 +802,52 @@ def test_earlier_hip_error_is_neither_blamed_nor_consumed():
     compare_fused(got, want, "after a failed hipMalloc")
 
 
+def test_tile_order_choice_keeps_results_and_a_pending_error():
+    """The first calls of a fused shape alternate between two tile orders and
+    time them with events the library polls: every call gives the same bits,
+    the order it settles on is one of the two, and while a caller's HIP error
+    is pending the polling leaves it in place (neither consumed nor replaced)."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    hip.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    rng = np.random.default_rng(909)
+    for n, use_error in ((1_000_003, False), (1_000_013, True)):
+        bks = random_buckets(rng, n, 3)
+        inp = random_inputs(rng, n, 4, 16)
+        announce("tile-order choice n=", n, "pending error:", use_error)
+        grads = [dev_f32(a) for a in inp["grads"]]
+        stale = [dev_bf16(a) for a in inp["stale"]]
+        x0, m0 = dev_f32(inp["params"]), dev_f32(inp["momentum"])
+        xs = [x0.clone() for _ in range(8)]
+        ms = [m0.clone() for _ in range(8)]
+        wires = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(8)]
+        sts = [daso.new_stats(len(bks)) for _ in range(8)]
+        steps = [daso.FusedStep(grads, xs[k], ms[k], stale, bks, 0.1, 0.9, 0.0, wire=wires[k], stats=sts[k])
+                 for k in range(8)]
+        cfg = steps[0].launch_config()
+        rule = cfg["xcd_run_tiles"]
+        torch.cuda.synchronize()
+        if use_error:
+            ptr = ctypes.c_void_p()
+            failed = hip.hipMalloc(ctypes.byref(ptr), ctypes.c_size_t(1 << 62))
+            assert failed != 0
+        for st in steps:
+            st()
+        if use_error:
+            assert hip.hipGetLastError() == failed     # still the caller's error
+            assert hip.hipGetLastError() == 0
+        torch.cuda.synchronize()
+        steps[0]()                                      # polls the samples, now complete
+        torch.cuda.synchronize()
+        chosen = steps[0].launch_config()["xcd_run_tiles"]
+        assert chosen in (rule, 1), (chosen, rule)
+        want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+        for k in range(1, 8):
+            got = {"params": host_f32(xs[k]), "momentum": host_f32(ms[k]), "wire": host_u16(wires[k]),
+                   "grad_avg": None, "stats": daso.decode_stats(sts[k])}
+            compare_fused(got, want, f"tile-order choice call {k}")
+
+
 def test_calls_from_several_host_threads():
     """Four host threads make fused calls with statistics at once, two of them
     on one shared stream: every call must still see its own tile partials (a
@@ -881,35 +927,42 @@ m = torch.randn(n, generator=gen, device="cuda") * 1e-3
 grads = [torch.randn(n, generator=gen, device="cuda") * 1e-3 for _ in range(g)]
 stale = [(x + torch.randn(n, generator=gen, device="cuda") * 1e-4).to(torch.bfloat16).view(torch.int16)
          for _ in range(P)]
-wire = torch.empty(n, dtype=torch.int16, device="cuda")
-st = daso.new_stats(len(bks))
-daso.fused_sync_step(grads, x, m, stale, bks, 0.1, 0.9, 0.0, wire, None, st)
-torch.cuda.synchronize()
-out = np.concatenate([x.cpu().numpy().view(np.uint8), m.cpu().numpy().view(np.uint8),
-                      wire.cpu().numpy().view(np.uint8), st.cpu().numpy().ravel().view(np.uint8)])
-sys.stdout.buffer.write(out.tobytes())
+outs = []
+for k in range(6):  # the first calls of a shape sample two tile orders, later ones take the chosen one
+    xk, mk = x.clone(), m.clone()
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    st = daso.new_stats(len(bks))
+    daso.fused_sync_step(grads, xk, mk, stale, bks, 0.1, 0.9, 0.0, wire, None, st)
+    torch.cuda.synchronize()
+    outs.append(np.concatenate([xk.cpu().numpy().view(np.uint8), mk.cpu().numpy().view(np.uint8),
+                                wire.cpu().numpy().view(np.uint8), st.cpu().numpy().ravel().view(np.uint8)]))
+assert all(np.array_equal(o, outs[0]) for o in outs), "calls of one process differ"
+sys.stdout.buffer.write(outs[0].tobytes())
 """
 
 
 @pytest.mark.parametrize("g,P", [(4, 8), (8, 32)])
 def test_launch_shape_never_changes_a_result(g, P):
-    """DASO_FUSED_RUN_ELEMS and DASO_FUSED_WG_PER_CU change only which XCD takes
-    which tiles and how many workgroups share a CU: plain order, the default
-    runs, longer or shorter runs, no occupancy cap and caps of 1 to 3 workgroups
-    per CU all give the same bits (2048- and 1024-element tiles)."""
+    """DASO_FUSED_RUN_ELEMS, DASO_FUSED_WG_PER_CU and DASO_FUSED_TUNE change only
+    which XCD takes which tiles and how many workgroups share a CU: plain order,
+    the default runs (chosen per shape from the first calls, or not), longer or
+    shorter runs, no occupancy cap and caps of 1 to 3 workgroups per CU all give
+    the same bits (2048- and 1024-element tiles)."""
     import os
     import subprocess
     import sys
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
     outs = {}
-    for run, cap in (("", ""), ("0", "0"), ("4096", "1"), ("65536", "3"), ("1048576", "2")):
-        announce("launch shape g=", g, "P=", P, "DASO_FUSED_RUN_ELEMS =", repr(run), "DASO_FUSED_WG_PER_CU =", repr(cap))
-        env = dict(os.environ, DASO_FUSED_RUN_ELEMS=run, DASO_FUSED_WG_PER_CU=cap)
+    for run, cap, tune in (("", "", ""), ("0", "0", ""), ("4096", "1", ""), ("65536", "3", ""),
+                           ("1048576", "2", ""), ("", "", "0")):
+        announce("launch shape g=", g, "P=", P, "DASO_FUSED_RUN_ELEMS =", repr(run), "DASO_FUSED_WG_PER_CU =",
+                 repr(cap), "DASO_FUSED_TUNE =", repr(tune))
+        env = dict(os.environ, DASO_FUSED_RUN_ELEMS=run, DASO_FUSED_WG_PER_CU=cap, DASO_FUSED_TUNE=tune)
         res = subprocess.run([sys.executable, "-c", _RUN_ORDER_SCRIPT, root, str(g), str(P)], capture_output=True,
                              env=env, timeout=110)
         assert res.returncode == 0, res.stderr.decode()[-2000:]
-        outs[(run, cap)] = res.stdout
-    base = outs[("", "")]
+        outs[(run, cap, tune)] = res.stdout
+    base = outs[("", "", "")]
     assert len(base) > 0
     for v, o in outs.items():
         assert o == base, v

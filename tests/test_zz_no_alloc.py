@@ -101,3 +101,42 @@ def test_noalloc_without_statistics_and_on_a_side_stream():
     assert np.array_equal(x.cpu().numpy().view(np.uint32), want["params"])
     assert np.array_equal(m.cpu().numpy().view(np.uint32), want["momentum"])
     assert np.array_equal(wire.cpu().numpy().view(np.uint16), want["wire"])
+
+
+def test_noalloc_captures_in_a_graph_on_a_fresh_stream():
+    """The fixed scratch needs no per-stream workspace, so the call can be
+    captured on a stream that has never run a fused step (an eager call on
+    another stream has looked up the scratch address on this device): every
+    replay, with eager work and synchronisations between replays, gives the
+    eager result bit for bit."""
+    inp, bks = _random_case(6, 400_003, 4, 8, 3)
+    n = inp["params"].numel()
+    want = _run(inp, bks, noalloc=False)
+    _same(_run(inp, bks, noalloc=True), want, "eager no-alloc call before the capture")
+    x0, m0 = inp["params"], inp["momentum"]
+    x, m = x0.clone(), m0.clone()
+    wire = torch.empty(n, dtype=torch.int16, device="cuda")
+    stats = daso.new_stats(len(bks))
+    step = daso.FusedStep(inp["grads"], x, m, inp["stale"], bks, 0.1, 0.9, 0.0, wire=wire, stats=stats,
+                          noalloc=True)
+    fresh = torch.cuda.Stream()
+    fresh.wait_stream(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=fresh):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        x.copy_(x0)
+        m.copy_(m0)
+        wire.fill_(0)
+        stats.zero_()
+        if rep == 1:   # other eager work on the device between replays
+            _run(inp, bks, noalloc=True)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(x.cpu().numpy().view(np.uint32), want["params"]), rep
+        assert np.array_equal(m.cpu().numpy().view(np.uint32), want["momentum"]), rep
+        assert np.array_equal(wire.cpu().numpy().view(np.uint16), want["wire"]), rep
+        assert np.array_equal(stats.cpu().numpy().view(np.uint64), want["stats"]), rep
