@@ -9,7 +9,6 @@
 #include <map>
 #include <mutex>
 #include <utility>
-#include <vector>
 
 #include "daso_host.h"
 #include "daso_launch.h"
@@ -99,16 +98,13 @@ struct Group {
   int64_t ntiles;
 };
 
-// Cut the caller's bucket table into launches of at most kLaunchBuckets buckets.
-std::vector<Group> group_buckets(const daso_bucket* b, int32_t nb, int64_t tile) {
-  std::vector<Group> out;
-  for (int32_t i = 0; i < nb; i += daso::kLaunchBuckets) {
-    Group gr{i, std::min<int32_t>(daso::kLaunchBuckets, nb - i), 0};
-    for (int32_t k = 0; k < gr.count; ++k)
-      gr.ntiles += daso::tiles_of(b[i + k].start, b[i + k].start + b[i + k].numel, tile);
-    out.push_back(gr);
-  }
-  return out;
+// The caller's bucket table is cut into launches of at most kLaunchBuckets
+// buckets; group(i) is the launch starting at bucket i (no allocation).
+Group group_at(const daso_bucket* b, int32_t nb, int32_t i, int64_t tile) {
+  Group gr{i, std::min<int32_t>(daso::kLaunchBuckets, nb - i), 0};
+  for (int32_t k = 0; k < gr.count; ++k)
+    gr.ntiles += daso::tiles_of(b[i + k].start, b[i + k].start + b[i + k].numel, tile);
+  return gr;
 }
 
 void fill_group(StepArgs& a, const daso_bucket* b, const Group& gr, int64_t tile) {
@@ -297,9 +293,20 @@ void try_decide(Tune& t, int32_t rule) {
     best[k % 2] = std::min(best[k % 2], ms);
   }
   t.chosen = best[1] < best[0] ? 1 : rule;
-  for (auto& e : t.ev)
-    for (hipEvent_t& x : e)
-      if (x) (void)hipEventDestroy(x), x = nullptr;
+  for (auto& e : t.ev) {
+    for (hipEvent_t& x : e) {
+      if (x) (void)hipEventDestroy(x);
+      x = nullptr;
+    }
+  }
+}
+
+// A failed HIP call made only for the sampling gives up sampling for the
+// shape; the error it left is dropped when no error was pending before it, so
+// that the library never leaves an error of its own behind.
+void give_up(Tune& t, bool was_clean) {
+  t.off = true;
+  if (was_clean && hipPeekAtLastError() != hipSuccess) (void)hipGetLastError();
 }
 
 // Where a fused launch with statistics keeps its tile partials and table.
@@ -312,9 +319,9 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
                daso_bucket_stats* stats, hipStream_t stream, Space space = Space::kAllocated) {
   const bool with_stats = (mode == daso::kModeFused) && stats != nullptr;
   const int64_t tile = daso::tile_elems(mode, with_stats, a);
-  const std::vector<Group> groups = group_buckets(b, nb, tile);
   int64_t max_tiles = 1;
-  for (const auto& gr : groups) {
+  for (int32_t i = 0; i < nb; i += daso::kLaunchBuckets) {
+    const Group gr = group_at(b, nb, i, tile);
     if (gr.ntiles > INT32_MAX) return DASO_EINVAL;
     max_tiles = std::max(max_tiles, gr.ntiles);
   }
@@ -347,9 +354,10 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(base) + table_at);
   }
   // the tile order of a single fused launch may be chosen per shape (above)
-  const bool choosable = mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams && groups.size() == 1 &&
-                         tuning_enabled();
-  for (const auto& gr : groups) {
+  const bool choosable = mode == daso::kModeFused && streams >= daso::kXcdRunFusedStreams &&
+                         nb <= daso::kLaunchBuckets && tuning_enabled();
+  for (int32_t i = 0; i < nb; i += daso::kLaunchBuckets) {
+    const Group gr = group_at(b, nb, i, tile);
     fill_group(a, b, gr, tile);
     a.stats = with_stats ? stats + gr.first : nullptr;
     const int32_t rule = xcd_run_of(mode, streams, a.ntiles, tile);
@@ -357,6 +365,7 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     Tune* t = nullptr;
     std::unique_lock<std::mutex> tl;
     hipEvent_t e0 = nullptr, e1 = nullptr;
+    bool clean = true;  // no HIP error was pending when sampling started
     if (choosable) {
       const TuneKey key = tune_key(dev, a, with_stats, b, nb);
       if (space == Space::kFixed) {
@@ -368,15 +377,18 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
         if (t->chosen > 0) {
           a.xcd_run = t->chosen;
         } else if (!t->off && t->taken < kTuneSamples) {
+          clean = hipPeekAtLastError() == hipSuccess;
           hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-          if (hipStreamIsCapturing(stream, &cs) == hipSuccess && cs == hipStreamCaptureStatusNone) {
+          if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+            give_up(*t, clean);
+          } else if (cs == hipStreamCaptureStatusNone) {
             hipEvent_t(&ev)[2] = t->ev[t->taken];
             if ((ev[0] || hipEventCreate(&ev[0]) == hipSuccess) && (ev[1] || hipEventCreate(&ev[1]) == hipSuccess)) {
               e0 = ev[0];
               e1 = ev[1];
               a.xcd_run = (t->taken % 2 == 0) ? rule : 1;
             } else {
-              t->off = true;
+              give_up(*t, clean);
             }
           }
         } else if (!t->off && t->taken == kTuneSamples) {
@@ -387,7 +399,7 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     }
     const int64_t grid = daso::host::launch_grid(a.ntiles, a.xcd_run);
     if (e0 && hipEventRecord(e0, stream) != hipSuccess) {
-      t->off = true;
+      give_up(*t, clean);
       e1 = nullptr;
     }
     if (daso::launch_step(mode, with_stats, a, static_cast<uint32_t>(grid), static_cast<uint32_t>(lds), stream) !=
@@ -397,7 +409,7 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
       if (hipEventRecord(e1, stream) == hipSuccess) {
         ++t->taken;
       } else {
-        t->off = true;
+        give_up(*t, clean);
       }
     }
   }
