@@ -451,6 +451,8 @@ def main() -> int:
                      # the resnet50-shaped target (80% of peak) is stated for the cold figure
                      "target": {"figure": "cold_frac", "frac": 0.80, "met": cold_frac >= 0.80},
                      "device_copy_GBps": copy_gbps,
+                     # the step's rate against a plain one-read one-write copy on the same box
+                     "frac_of_copy": achieved / copy_gbps,
                      "ceiling": ceil},
         "entry_points": entry_points,
         "graph_replay": graph_replay,
