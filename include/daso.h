@@ -67,7 +67,8 @@
  *    single launch (up to 64 buckets), the first 4 calls of
  *    daso_fused_sync_step alternate between those runs and plain tile order,
  *    timed with events on the call's stream that later calls poll (never wait
- *    on); once they have completed, the faster order is kept for the shape.
+ *    on); once they have completed, plain order is kept for the shape if it
+ *    was at least 1% faster, the runs otherwise.
  *    Captured calls take no samples, and polling is skipped while a HIP error
  *    is pending on the calling thread, so that error stays for the caller.
  *    The environment variables DASO_FUSED_RUN_ELEMS (elements per run, 0 =

@@ -195,12 +195,14 @@ int current_device(hipStream_t stream, int* dev) {
 // fused launch shape of a single launch, the first kTuneSamples calls alternate
 // between the rule's run length and plain order, each bracketed by two events
 // on the call's stream.  Once the last of them has completed, which later calls
-// poll with hipEventQuery (never waiting), the order with the shorter fastest
-// sample is kept for the shape; until then calls take the rule's run length.
+// poll with hipEventQuery (never waiting), plain order is kept for the shape if
+// its fastest sample beat the rule's by at least 1%, the rule's runs otherwise;
+// until then calls take the rule's run length.
 // The order never changes a result.  No sample is taken by a captured call, by
 // daso_fused_sync_step_noalloc (it only reads a choice already made), or when
 // DASO_FUSED_RUN_ELEMS or DASO_FUSED_TUNE=0 is set.
-constexpr int kTuneSamples = 4;  // rule, plain, rule, plain
+constexpr int kTuneSamples = 4;             // rule, plain, rule, plain
+constexpr float kTunePlainMargin = 0.99f;   // plain order must be at least 1% faster
 
 bool tuning_enabled() {
   static const bool v = env_count("DASO_FUSED_TUNE", 1, 1) != 0 && fused_run_elems_override() < 0;
@@ -292,7 +294,9 @@ void try_decide(Tune& t, int32_t rule) {
     }
     best[k % 2] = std::min(best[k % 2], ms);
   }
-  t.chosen = best[1] < best[0] ? 1 : rule;
+  // plain order only when it measured clearly faster: the rule's runs are the
+  // measured default, and two samples each cannot separate closer orders
+  t.chosen = best[1] < kTunePlainMargin * best[0] ? 1 : rule;
   for (auto& e : t.ev) {
     for (hipEvent_t& x : e) {
       if (x) (void)hipEventDestroy(x);
