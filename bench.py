@@ -238,7 +238,7 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (the DASO sync step runs on one GPU's "
+        print(f"bench.py: measures one GPU only (the DASO sync step runs on one GPU's "
               f"share with peer copies resident in HBM); --gpus {args.gpus} is not supported",
               file=sys.stderr)
         return 2
