@@ -144,7 +144,8 @@ def ceiling(torch, probes, w, inp, wire, step, reps):
     """The step and its access pattern on the step's own buffers, tile grid, tile
     order and occupancy cap, each cold (cache evicted before every call) and warm (back to
     back): the reads alone (g + 2 fp32 and P bf16 streams), the writes alone
-    (params and momentum fp32, the wire bf16), both mixed as a bare kernel, and
+    (params and momentum fp32, the wire bf16), both mixed as a bare kernel (for the
+    g = 4, P = 8 shape also with bf16 at 16 bytes per lane, in two layouts), and
     the separated bound = reads alone + writes alone."""
     n = w.n
     cfg = step.launch_config()  # the step's own tile size, tile order and occupancy cap
@@ -160,6 +161,11 @@ def ceiling(torch, probes, w, inp, wire, step, reps):
            "reads_alone": probes.call(rd32, rd16, [], [], n, it, run, lds),
            "writes_alone": probes.call([], [], wr32, wr16, n, it, run, lds),
            "bare_mix": probes.call(rd32, rd16, wr32, wr16, n, it, run, lds)}
+    if (len(rd32), len(rd16)) == (6, 8) and tile == 2048 and n % 8 == 0:
+        # the same mix with bf16 at 16 bytes per lane: each lane its own 8 elements
+        # (fp32 at a 32-byte lane stride), and fp32 left as the step takes it
+        fns["bare_mix_8_per_lane"] = probes.call(rd32, rd16, wr32, wr16, n, 0, run, lds)
+        fns["bare_mix_bf16_16B"] = probes.call(rd32, rd16, wr32, wr16, n, -1, run, lds)
     out = {"tile_elems": tile, "xcd_run_tiles": run, "lds_bytes": lds, "read_bytes": read_b,
            "write_bytes": write_b}
     for name, fn in fns.items():
@@ -167,7 +173,10 @@ def ceiling(torch, probes, w, inp, wire, step, reps):
         out[name] = {"cold_median_us": med, "cold_min_us": mn, "warm_us": time_warm(torch, fn, reps)}
     del scratch
     for name, b in (("reads_alone", read_b), ("writes_alone", write_b), ("bare_mix", read_b + write_b),
+                    ("bare_mix_8_per_lane", read_b + write_b), ("bare_mix_bf16_16B", read_b + write_b),
                     ("step", read_b + write_b)):
+        if name not in out:
+            continue
         out[name]["cold_GBps"] = b / (out[name]["cold_median_us"] * 1e-6) / 1e9
     sep = out["reads_alone"]["cold_median_us"] + out["writes_alone"]["cold_median_us"]
     sep_warm = out["reads_alone"]["warm_us"] + out["writes_alone"]["warm_us"]

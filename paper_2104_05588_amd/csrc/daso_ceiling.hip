@@ -7,13 +7,15 @@
 // of its arithmetic: R32 fp32 and R16 bf16 streams read, W32 fp32 and W16 bf16
 // streams written.  Taking the reads alone, the writes alone and both mixed,
 // they measure what the step's access mix can reach on a given part; a one-
-// stream copy gives the plain copy rate.
+// stream copy gives the plain copy rate.  Two more mixed probes take bf16 at 16
+// bytes per lane, to price the wider bf16 access.
 //
-// Safety: every stream holds at least n elements and n is a multiple of 4
-// (checked by daso_probe_run before any launch), so a thread touches the
-// 4-element vector at element e0 only when e0 < n, which keeps the whole vector
-// inside every buffer.  The grid is at most the tile count, each workgroup
-// looping over tiles grid apart, so every tile is visited once.
+// Safety: every stream holds at least n elements and n is a multiple of 4, of 8
+// for the 16-byte bf16 probes (checked by daso_probe_run before any launch), so a
+// thread touches the vector at element e0 only when e0 < n, which keeps the
+// whole vector inside every buffer.  The grid is at most the tile count of the
+// probe's own tile size, each workgroup looping over tiles grid apart, so every
+// tile is visited once.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -34,7 +36,7 @@ struct ProbeArgs {
   void* wr32[kMaxWrite];       // fp32 streams written
   void* wr16[kMaxWrite];       // bf16 streams written
   uint32_t* sink;              // one word: a read-only probe stores its fold here when sink_flag != 0
-  int64_t n;                   // elements per stream, a multiple of 4
+  int64_t n;                   // elements per stream, a multiple of 4 (of 8 for the 16-byte bf16 probes)
   int32_t ntiles;
   int32_t xcd_run;
   int32_t sink_flag;           // 0 in every run; keeps the loads of a read-only probe alive
@@ -88,11 +90,76 @@ __global__ __launch_bounds__(kProbeBlock) void probe_kernel(const ProbeArgs a) {
   }
 }
 
+// The same mix on 2048-element tiles with bf16 accessed at 16 bytes per lane,
+// in two forms.  SAME: each lane takes its own 8 consecutive elements, fp32 as
+// two adjacent 16-byte accesses (a 32-byte stride between lanes), bf16 as one
+// 16-byte access: the layout a step would need to keep a lane's elements
+// together.  !SAME: fp32 as the step takes it (lane i at elements 4i and
+// 1024 + 4i of the tile, every access contiguous across the wavefront), bf16 at
+// elements 8i to 8i + 7: a lane then holds different elements of the two types,
+// which a step would have to exchange between lanes; this bounds what the wider
+// bf16 access alone could give.  Every stream holds at least n elements and n
+// is a multiple of 8, so each guarded vector lies inside its buffer.
+template <int R32, int R16, int W32, int W16, bool SAME>
+__global__ __launch_bounds__(kProbeBlock) void probe_wide_kernel(const ProbeArgs a) {
+  constexpr int64_t kTile = int64_t(kProbeBlock) * 8;
+  const int w0 = a.xcd_run > 1 ? daso::xcd_runs(static_cast<int>(blockIdx.x), static_cast<int>(gridDim.x), a.xcd_run)
+                               : static_cast<int>(blockIdx.x);
+  for (int64_t t = w0; t < a.ntiles; t += gridDim.x) {
+    const int64_t e16 = t * kTile + int64_t(threadIdx.x) * 8;  // the lane's bf16 vector
+    int64_t e32[2];                                             // the lane's fp32 vectors
+    e32[0] = SAME ? e16 : t * kTile + int64_t(threadIdx.x) * 4;
+    e32[1] = SAME ? e16 + 4 : e32[0] + int64_t(kProbeBlock) * 4;
+    const bool in16 = e16 < a.n, in32[2] = {e32[0] < a.n, e32[1] < a.n};
+    u32x4 r32[R32 > 0 ? R32 : 1][2];
+    u32x4 r16[R16 > 0 ? R16 : 1];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      if (in32[h]) {
+#pragma unroll
+        for (int s = 0; s < R32; ++s)
+          r32[s][h] = __builtin_nontemporal_load(static_cast<const u32x4*>(a.rd32[s]) + e32[h] / 4);
+      }
+    if (in16) {
+#pragma unroll
+      for (int s = 0; s < R16; ++s) r16[s] = __builtin_nontemporal_load(static_cast<const u32x4*>(a.rd16[s]) + e16 / 8);
+    }
+    u32x4 v[2] = {{static_cast<uint32_t>(e16), 1u, 2u, 3u}, {static_cast<uint32_t>(e16), 5u, 6u, 7u}};
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      if (in32[h]) {
+#pragma unroll
+        for (int s = 0; s < R32; ++s) v[h] ^= r32[s][h];
+      }
+    u32x4 v16 = v[0] ^ v[1];
+    if (in16) {
+#pragma unroll
+      for (int s = 0; s < R16; ++s) v16 ^= r16[s];
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+      if (in32[h]) {
+#pragma unroll
+        for (int w = 0; w < W32; ++w) __builtin_nontemporal_store(v[h] ^ v16, static_cast<u32x4*>(a.wr32[w]) + e32[h] / 4);
+      }
+    if (in16) {
+#pragma unroll
+      for (int w = 0; w < W16; ++w) __builtin_nontemporal_store(v16, static_cast<u32x4*>(a.wr16[w]) + e16 / 8);
+    }
+  }
+}
+
 template <int R32, int R16, int W32, int W16, int ITERS>
 hipError_t launch(const ProbeArgs& a, uint32_t grid, uint32_t lds, hipStream_t stream) {
   void* args[] = {const_cast<ProbeArgs*>(&a)};
-  return hipLaunchKernel(reinterpret_cast<const void*>(&probe_kernel<R32, R16, W32, W16, ITERS>), dim3(grid),
-                         dim3(kProbeBlock), args, lds, stream);
+  const void* k;
+  if constexpr (ITERS == 0)
+    k = reinterpret_cast<const void*>(&probe_wide_kernel<R32, R16, W32, W16, true>);
+  else if constexpr (ITERS == -1)
+    k = reinterpret_cast<const void*>(&probe_wide_kernel<R32, R16, W32, W16, false>);
+  else
+    k = reinterpret_cast<const void*>(&probe_kernel<R32, R16, W32, W16, ITERS>);
+  return hipLaunchKernel(k, dim3(grid), dim3(kProbeBlock), args, lds, stream);
 }
 
 // The access shapes of the fused step on the five workloads (g + 2 fp32 reads,
@@ -105,7 +172,8 @@ hipError_t launch(const ProbeArgs& a, uint32_t grid, uint32_t lds, hipStream_t s
   X(6, 8, 2, 1, 2) X(6, 8, 0, 0, 2)                    /* g=4, P=8  */        \
   X(6, 16, 2, 1, 1) X(6, 16, 0, 0, 1) X(0, 0, 2, 1, 1) /* g=4, P=16 */        \
   X(10, 32, 2, 1, 1) X(10, 32, 0, 0, 1)                /* g=8, P=32 */        \
-  X(1, 0, 1, 0, 2)                                     /* copy      */
+  X(1, 0, 1, 0, 2)                                     /* copy      */        \
+  X(6, 8, 2, 1, 0) X(6, 8, 2, 1, -1)                   /* g=4, P=8, bf16 16 B */
 
 }  // namespace
 
@@ -113,14 +181,17 @@ extern "C" {
 
 // Runs one probe: r32/r16 read streams and w32/w16 written streams (host arrays
 // of device pointers, each stream at least n elements of 4 or 2 bytes), tiles of
-// 1024 * iters elements in runs of xcd_run tiles per XCD, each workgroup holding
+// 1024 * iters elements (iters 1 or 2, 4-element vectors; iters 0 and -1: the
+// two 16-byte bf16 forms of probe_wide_kernel, SAME and not, on 2048-element
+// tiles, n a multiple of 8) in runs of xcd_run tiles per XCD, each workgroup holding
 // lds_bytes of (unused) LDS, which caps how many share a CU, as the step's
 // launches do.  Returns 0, -1 for a shape without an instance or invalid
 // sizes/pointers, -4 when the launch fails.  Nothing is launched on -1.
 int daso_probe_run(const void* const* rd32, int32_t r32, const void* const* rd16, int32_t r16, void* const* wr32,
                    int32_t w32, void* const* wr16, int32_t w16, uint32_t* sink, int64_t n, int32_t iters,
                    int32_t xcd_run, int32_t lds_bytes, hipStream_t stream) {
-  if (n <= 0 || n % 4 != 0 || (iters != 1 && iters != 2) || xcd_run < 1 || sink == nullptr) return -1;
+  if (n <= 0 || n % 4 != 0 || iters < -1 || iters > 2 || xcd_run < 1 || sink == nullptr) return -1;
+  if (iters <= 0 && n % 8 != 0) return -1;
   if (lds_bytes < 0 || lds_bytes > 160 * 1024) return -1;
   if (r32 < 0 || r32 > kMaxRead || r16 < 0 || r16 > kMaxRead || w32 < 0 || w32 > kMaxWrite || w16 < 0 ||
       w16 > kMaxWrite)
@@ -142,7 +213,7 @@ int daso_probe_run(const void* const* rd32, int32_t r32, const void* const* rd16
     if (wr16 == nullptr || wr16[i] == nullptr || (reinterpret_cast<uintptr_t>(wr16[i]) & 15u)) return -1;
     a.wr16[i] = wr16[i];
   }
-  const int64_t tile = int64_t(kProbeBlock) * 4 * iters;
+  const int64_t tile = int64_t(kProbeBlock) * (iters <= 0 ? 8 : 4 * iters);
   const int64_t ntiles = (n + tile - 1) / tile;
   if (ntiles > INT32_MAX) return -1;
   a.sink = sink;
