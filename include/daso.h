@@ -64,11 +64,12 @@
  *    (about 64 blocks of 8 runs per launch from 9 streams) and, from 10
  *    streams, lets at most 2 workgroups share a CU; both were measured best on
  *    MI355X (daso_fused_launch_config reports them).  For each shape of a
- *    single launch (up to 64 buckets), the first 4 calls of
- *    daso_fused_sync_step alternate between those runs and plain tile order,
+ *    single launch (up to 64 buckets), the 6 calls of daso_fused_sync_step
+ *    after its first alternate between those runs and plain tile order,
  *    timed with events on the call's stream that later calls poll (never wait
- *    on); once they have completed, plain order is kept for the shape if it
- *    was at least 1% faster, the runs otherwise.
+ *    on); once all of them have completed (samples may be taken on different
+ *    streams), plain order is kept for the shape if it was at least 1% faster,
+ *    the runs otherwise.
  *    Captured calls take no samples, and polling is skipped while a HIP error
  *    is pending on the calling thread, so that error stays for the caller.
  *    The environment variables DASO_FUSED_RUN_ELEMS (elements per run, 0 =

@@ -192,16 +192,19 @@ int current_device(hipStream_t stream, int* dev) {
 // ----------------------------------------------------------- tile-order choice
 // The rule's run length is the best measured for most fused shapes, but some
 // (the segmentation-shaped step) run 2 to 5% faster in plain order.  For each
-// fused launch shape of a single launch, the first kTuneSamples calls alternate
-// between the rule's run length and plain order, each bracketed by two events
-// on the call's stream.  Once the last of them has completed, which later calls
-// poll with hipEventQuery (never waiting), plain order is kept for the shape if
-// its fastest sample beat the rule's by at least 1%, the rule's runs otherwise;
-// until then calls take the rule's run length.
+// fused launch shape of a single launch, the first call is left out (it can
+// carry one-off costs: the first launch of a kernel in a process takes
+// milliseconds), then kTuneSamples calls alternate between the rule's run
+// length and plain order, each bracketed by two events on the call's stream.
+// Once all of them have completed, which later calls poll with hipEventQuery
+// (never waiting), plain order is kept for the shape if its fastest sample beat
+// the rule's by at least 1%, the rule's runs otherwise; until then calls take
+// the rule's run length.
 // The order never changes a result.  No sample is taken by a captured call, by
 // daso_fused_sync_step_noalloc (it only reads a choice already made), or when
 // DASO_FUSED_RUN_ELEMS or DASO_FUSED_TUNE=0 is set.
-constexpr int kTuneSamples = 4;             // rule, plain, rule, plain
+constexpr int kTuneSkip = 1;                // calls of a shape before sampling starts
+constexpr int kTuneSamples = 6;             // rule, plain, rule, plain, rule, plain
 constexpr float kTunePlainMargin = 0.99f;   // plain order must be at least 1% faster
 
 bool tuning_enabled() {
@@ -229,6 +232,7 @@ struct TuneKey {
 struct Tune {
   std::mutex mu;
   hipEvent_t ev[kTuneSamples][2] = {};
+  int skipped = 0;     // calls left out before the first sample
   int taken = 0;       // samples whose launches are queued
   int32_t chosen = 0;  // tiles per run once decided, 0 before
   bool off = false;    // an event call failed: keep the rule for this shape
@@ -273,14 +277,16 @@ Tune& tune_entry(const TuneKey& k) {
   return g_tune[k];
 }
 
-// With t.mu held, after all samples were queued: decide once the last has
-// completed.  The query runs only when no error is pending on this thread, and
-// the not-ready status it may leave is cleared, so a caller's error is neither
-// consumed nor masked.
+// With t.mu held, after all samples were queued: decide once every sample has
+// completed (calls of one shape may sample on different streams, so the last
+// queued need not be the last to finish).  The queries run only when no error
+// is pending on this thread, and any status they leave is cleared, so a
+// caller's error is neither consumed nor masked and none is left behind.
 void try_decide(Tune& t, int32_t rule) {
   if (hipPeekAtLastError() != hipSuccess) return;
-  const hipError_t q = hipEventQuery(t.ev[kTuneSamples - 1][1]);
-  if (q != hipSuccess) {
+  for (int k = 0; k < kTuneSamples; ++k) {
+    const hipError_t q = hipEventQuery(t.ev[k][1]);
+    if (q == hipSuccess) continue;
     if (hipPeekAtLastError() != hipSuccess) (void)hipGetLastError();
     if (q != hipErrorNotReady) t.off = true;
     return;
@@ -289,6 +295,7 @@ void try_decide(Tune& t, int32_t rule) {
   for (int k = 0; k < kTuneSamples; ++k) {
     float ms = 0.0f;
     if (hipEventElapsedTime(&ms, t.ev[k][0], t.ev[k][1]) != hipSuccess) {
+      if (hipPeekAtLastError() != hipSuccess) (void)hipGetLastError();
       t.off = true;
       return;
     }
@@ -380,6 +387,8 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
         tl = std::unique_lock<std::mutex>(t->mu);
         if (t->chosen > 0) {
           a.xcd_run = t->chosen;
+        } else if (!t->off && t->skipped < kTuneSkip) {
+          ++t->skipped;
         } else if (!t->off && t->taken < kTuneSamples) {
           clean = hipPeekAtLastError() == hipSuccess;
           hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;

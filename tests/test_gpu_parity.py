@@ -848,6 +848,59 @@ def test_tile_order_choice_keeps_results_and_a_pending_error():
             compare_fused(got, want, f"tile-order choice call {k}")
 
 
+def test_tile_order_samples_on_two_streams_finishing_out_of_order():
+    """After a shape's first call, its six sampled calls alternate between two
+    streams; the first stream is kept busy, so the later samples on the second
+    one finish first.  A call that polls then must not read the unfinished
+    samples' times or leave a HIP error behind; a later poll decides, and every
+    call gives the oracle's bits."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    rng = np.random.default_rng(919)
+    n = 1_000_033
+    bks = random_buckets(rng, n, 3)
+    inp = random_inputs(rng, n, 4, 16)
+    announce("tile-order samples on two streams, n=", n)
+    grads = [dev_f32(a) for a in inp["grads"]]
+    stale = [dev_bf16(a) for a in inp["stale"]]
+    x0, m0 = dev_f32(inp["params"]), dev_f32(inp["momentum"])
+    sampled = 1 + 6                       # the unsampled first call, then the samples
+    calls = sampled + 2
+    xs = [x0.clone() for _ in range(calls)]
+    ms = [m0.clone() for _ in range(calls)]
+    wires = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(calls)]
+    sts = [daso.new_stats(len(bks)) for _ in range(calls)]
+    steps = [daso.FusedStep(grads, xs[k], ms[k], stale, bks, 0.1, 0.9, 0.0, wire=wires[k], stats=sts[k])
+             for k in range(calls)]
+    rule = steps[0].launch_config()["xcd_run_tiles"]
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    busy = torch.empty(1 << 29, dtype=torch.float32, device="cuda")   # 2 GiB
+    torch.cuda.synchronize()
+    for k in range(sampled):              # odd calls on the first stream, the last sample on the second
+        s = sa if k % 2 == 1 else sb
+        with torch.cuda.stream(s):
+            if s is sa:
+                for i in range(6):        # a few ms of fills ahead of each sample on the first stream
+                    busy.fill_(float(i))
+            steps[k]()
+    sb.synchronize()                      # the second stream's samples are done
+    with torch.cuda.stream(sb):
+        steps[sampled]()                  # polls while the first stream's samples are still queued
+    assert hip.hipPeekAtLastError() == 0
+    torch.cuda.synchronize()
+    with torch.cuda.stream(sb):
+        steps[sampled + 1]()              # polls again: every sample has completed
+    torch.cuda.synchronize()
+    assert hip.hipGetLastError() == 0
+    assert steps[0].launch_config()["xcd_run_tiles"] in (rule, 1)
+    del busy
+    want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+    for k in range(calls):
+        got = {"params": host_f32(xs[k]), "momentum": host_f32(ms[k]), "wire": host_u16(wires[k]),
+               "grad_avg": None, "stats": daso.decode_stats(sts[k])}
+        compare_fused(got, want, f"two-stream sampling call {k}")
+
+
 def test_calls_from_several_host_threads():
     """Four host threads make fused calls with statistics at once, two of them
     on one shared stream: every call must still see its own tile partials (a
@@ -928,7 +981,7 @@ grads = [torch.randn(n, generator=gen, device="cuda") * 1e-3 for _ in range(g)]
 stale = [(x + torch.randn(n, generator=gen, device="cuda") * 1e-4).to(torch.bfloat16).view(torch.int16)
          for _ in range(P)]
 outs = []
-for k in range(6):  # the first calls of a shape sample two tile orders, later ones take the chosen one
+for k in range(10):  # after its first call a shape samples two tile orders (6 calls), later ones take the chosen one
     xk, mk = x.clone(), m.clone()
     wire = torch.empty(n, dtype=torch.int16, device="cuda")
     st = daso.new_stats(len(bks))
