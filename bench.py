@@ -82,6 +82,32 @@ class Probes:
             arr[i] = t.data_ptr()
         return arr
 
+    def phased(self, rd32, rd16, wr32, wr16, n, iters, nwg, spin_limit=100_000):
+        """A callable that runs the chip-wide phased probe once on the current
+        stream; it returns how many of its waits gave up so far."""
+        lib, ct, torch = self.lib, self.ct, self.torch
+        if not hasattr(self, "_phased_ready"):
+            vp, i32, i64 = ct.c_void_p, ct.c_int32, ct.c_int64
+            lib.daso_probe_phased.argtypes = [ct.POINTER(vp), i32, ct.POINTER(vp), i32, ct.POINTER(vp),
+                                              ct.POINTER(vp), vp, vp, i64, i32, i32, i32, vp]
+            lib.daso_probe_phased.restype = ct.c_int
+            self.ctr = torch.zeros(4, dtype=torch.int32, device="cuda")
+            self.late = torch.zeros(4, dtype=torch.int32, device="cuda")
+            self._phased_ready = True
+        if len(wr32) != 2 or len(wr16) != 1:
+            raise ValueError("the phased probe writes the step's three streams")
+        args = (self._arr(rd32, n, 4), len(rd32), self._arr(rd16, n, 2), len(rd16), self._arr(wr32, n, 4),
+                self._arr(wr16, n, 2), ct.c_void_p(self.ctr.data_ptr()), ct.c_void_p(self.late.data_ptr()),
+                ct.c_int64(n), iters, nwg, spin_limit)
+        keep = (rd32, rd16, wr32, wr16)
+
+        def run():
+            _ = keep
+            rc = lib.daso_probe_phased(*args, ct.c_void_p(torch.cuda.current_stream().cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"daso_probe_phased failed with {rc}")
+        return run
+
     def call(self, rd32, rd16, wr32, wr16, n, iters, xcd_run, lds=0):
         """A callable that launches the probe once on the current stream."""
         args = (self._arr(rd32, n, 4), len(rd32), self._arr(rd16, n, 2), len(rd16), self._arr(wr32, n, 4),
@@ -188,6 +214,39 @@ def ceiling(torch, probes, w, inp, wire, step, reps):
     return out
 
 
+def phased(torch, probes, w, inp, wire, step, reps):
+    """Reads and writes separated across the whole chip, made real: the phased
+    probe (every workgroup reads its tiles into LDS, all meet, all write, all
+    meet again) beside the bare mix, the reads alone and the writes alone, on
+    the step's own buffers, cold and warm."""
+    n = w.n
+    it = step.launch_config()["tile_elems"] // 1024
+    rd32 = list(inp["grads"]) + [inp["params"], inp["momentum"]]
+    rd16 = list(inp["stale"])
+    wr32, wr16 = [inp["params"], inp["momentum"]], [wire]
+    cfg = step.launch_config()
+    run, lds = cfg["xcd_run_tiles"], cfg["lds_bytes"]
+    nwg = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    read_b, write_b = n * (4 * len(rd32) + 2 * len(rd16)), n * 10
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    fns = {"step": step,
+           "bare_mix": probes.call(rd32, rd16, wr32, wr16, n, it, run, lds),
+           "reads_alone": probes.call(rd32, rd16, [], [], n, it, run, lds),
+           "writes_alone": probes.call([], [], wr32, wr16, n, it, run, lds),
+           "phased": probes.phased(rd32, rd16, wr32, wr16, n, it, nwg)}
+    out = {"workgroups": nwg, "read_bytes": read_b, "write_bytes": write_b}
+    for name, fn in fns.items():
+        med, mn = time_cold(torch, fn, reps, scratch)
+        out[name] = {"cold_median_us": med, "cold_min_us": mn, "warm_us": time_warm(torch, fn, reps)}
+        b = read_b if name == "reads_alone" else (write_b if name == "writes_alone" else read_b + write_b)
+        out[name]["cold_GBps"] = b / (med * 1e-6) / 1e9
+    del scratch
+    torch.cuda.synchronize()
+    out["phased_waits_given_up"] = int(probes.late[0])
+    out["separated_bound_cold_us"] = out["reads_alone"]["cold_median_us"] + out["writes_alone"]["cold_median_us"]
+    return out
+
+
 def cpu_baseline(w, budget_s: float):
     """The CPU oracle, as it is, on a bounded sample: the first bucket of the
     workload, stepped over and over, first on one host thread (a third of
@@ -238,6 +297,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run only a plain 1 GiB device copy, --steps times (counter calibration)")
+    ap.add_argument("--phased", action="store_true",
+                    help="time only the step beside the chip-wide phased probe (reads, then writes, all workgroups "
+                         "meeting between the phases), the bare mix, the reads alone and the writes alone")
     ap.add_argument("--ceiling", action="store_true",
                     help="time only the step and its access-pattern probes (reads alone, writes alone, bare "
                          "mix; --steps calls each, cold and warm) and a 1 GiB copy; prints one JSON line")
@@ -292,6 +354,12 @@ def main() -> int:
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+
+    if args.phased:
+        ph = phased(torch, probes, w, inp, wire, step, max(3, min(args.steps, 20)))
+        print(json.dumps({"workload": f"{w.name}-shaped parameter set", "params": n, "g": w.g, "P": w.P,
+                          "phased": ph, "peak_GBps": PEAK_HBM_GBPS}), flush=True)
+        return 0
 
     if args.ceiling:
         ceil = ceiling(torch, probes, w, inp, wire, step, max(5, min(args.steps, 50)))

@@ -8,7 +8,8 @@
 // streams written.  Taking the reads alone, the writes alone and both mixed,
 // they measure what the step's access mix can reach on a given part; a one-
 // stream copy gives the plain copy rate.  Two more mixed probes take bf16 at 16
-// bytes per lane, to price the wider bf16 access.
+// bytes per lane, to price the wider bf16 access, and a phased probe separates
+// reads from writes across the whole chip, as the separated bound assumes.
 //
 // Safety: every stream holds at least n elements and n is a multiple of 4, of 8
 // for the 16-byte bf16 probes (checked by daso_probe_run before any launch), so a
@@ -149,6 +150,109 @@ __global__ __launch_bounds__(kProbeBlock) void probe_wide_kernel(const ProbeArgs
   }
 }
 
+// Reads and writes separated across the whole chip: every workgroup reads K
+// tiles of the step's mix (the values of probe_kernel<R32, R16, 2, 1, ITERS>)
+// into LDS, all workgroups meet, every workgroup writes its K tiles' outputs,
+// all meet again, and so on.  This is the schedule the separated bound assumes,
+// made real.  The meeting is a counter in device memory that every workgroup
+// raises once per meeting (an agent-scope atomic add) and then polls; a wait
+// longer than spin_limit polls gives up, counts itself in *late and goes on, so
+// every wait ends even if some workgroup were never to arrive.  The launch is
+// cooperative, so all workgroups are resident at once.  Every workgroup runs
+// the same number of rounds and meetings; tile t of round r is r * gridDim.x * K
+// + blockIdx.x * K + k, each guarded by the tile count and the element count.
+struct PhasedArgs {
+  ProbeArgs p;
+  uint32_t* ctr;   // meeting counter, zeroed before the launch
+  uint32_t* late;  // waits that gave up
+  int32_t spin_limit;
+};
+
+__device__ __forceinline__ void meet(const PhasedArgs& a, uint32_t target) {
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __hip_atomic_fetch_add(a.ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    int32_t polls = 0;
+    while (__hip_atomic_load(a.ctr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+      if (++polls > a.spin_limit) {
+        __hip_atomic_fetch_add(a.late, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+}
+
+template <int R32, int R16, int ITERS, int K>
+__global__ __launch_bounds__(kProbeBlock) void phased_kernel(const PhasedArgs a) {
+  extern __shared__ u32x4 staged[];  // [K][ITERS][kProbeBlock]
+  constexpr int64_t kTile = int64_t(kProbeBlock) * 4 * ITERS;
+  const ProbeArgs& q = a.p;
+  uint32_t met = 0;
+  for (int64_t base = 0; base < q.ntiles; base += int64_t(gridDim.x) * K) {
+#pragma unroll 1
+    for (int k = 0; k < K; ++k) {
+      const int64_t t = base + int64_t(blockIdx.x) * K + k;
+      if (t >= q.ntiles) break;
+      u32x4 r32[ITERS][R32];
+      u32x2 r16[ITERS][R16];
+#pragma unroll
+      for (int it = 0; it < ITERS; ++it) {
+        const int64_t e0 = t * kTile + int64_t(threadIdx.x) * 4 + int64_t(it) * kProbeBlock * 4;
+        if (e0 < q.n) {
+#pragma unroll
+          for (int s = 0; s < R32; ++s)
+            r32[it][s] = __builtin_nontemporal_load(static_cast<const u32x4*>(q.rd32[s]) + e0 / 4);
+#pragma unroll
+          for (int s = 0; s < R16; ++s)
+            r16[it][s] = __builtin_nontemporal_load(static_cast<const u32x2*>(q.rd16[s]) + e0 / 4);
+        }
+      }
+#pragma unroll
+      for (int it = 0; it < ITERS; ++it) {
+        const int64_t e0 = t * kTile + int64_t(threadIdx.x) * 4 + int64_t(it) * kProbeBlock * 4;
+        if (e0 >= q.n) continue;
+        u32x4 v = {static_cast<uint32_t>(e0), 1u, 2u, 3u};
+#pragma unroll
+        for (int s = 0; s < R32; ++s) v ^= r32[it][s];
+#pragma unroll
+        for (int s = 0; s < R16; ++s) {
+          v.x ^= r16[it][s].x;
+          v.y ^= r16[it][s].y;
+        }
+        staged[(k * ITERS + it) * kProbeBlock + threadIdx.x] = v;
+      }
+    }
+    met += gridDim.x;
+    meet(a, met);
+#pragma unroll 1
+    for (int k = 0; k < K; ++k) {
+      const int64_t t = base + int64_t(blockIdx.x) * K + k;
+      if (t >= q.ntiles) break;
+#pragma unroll
+      for (int it = 0; it < ITERS; ++it) {
+        const int64_t e0 = t * kTile + int64_t(threadIdx.x) * 4 + int64_t(it) * kProbeBlock * 4;
+        if (e0 >= q.n) continue;
+        const u32x4 v = staged[(k * ITERS + it) * kProbeBlock + threadIdx.x];
+        __builtin_nontemporal_store(v, static_cast<u32x4*>(q.wr32[0]) + e0 / 4);
+        __builtin_nontemporal_store(v, static_cast<u32x4*>(q.wr32[1]) + e0 / 4);
+        const u32x2 h = {v.x, v.y};
+        __builtin_nontemporal_store(h, static_cast<u32x2*>(q.wr16[0]) + e0 / 4);
+      }
+    }
+    met += gridDim.x;
+    meet(a, met);
+  }
+}
+
+// Tiles staged per workgroup and round: as many as fit 72 KB of LDS, so that
+// two workgroups share a CU as in the step's launches.
+template <int ITERS>
+constexpr int phased_tiles() {
+  return (72 * 1024) / (ITERS * kProbeBlock * 16);
+}
+
 template <int R32, int R16, int W32, int W16, int ITERS>
 hipError_t launch(const ProbeArgs& a, uint32_t grid, uint32_t lds, hipStream_t stream) {
   void* args[] = {const_cast<ProbeArgs*>(&a)};
@@ -231,6 +335,66 @@ int daso_probe_run(const void* const* rd32, int32_t r32, const void* const* rd16
   DASO_PROBE_SHAPES(DASO_PROBE_CASE)
 #undef DASO_PROBE_CASE
   return -1;
+}
+
+// Runs phased_kernel over r32 fp32 and r16 bf16 read streams and the step's
+// three written streams (wr32[0..1] fp32, wr16[0] bf16), each at least n
+// elements (n a multiple of 4), on nwg workgroups (a cooperative launch: all of
+// them resident at once, else the launch fails).  iters as in daso_probe_run
+// (1 or 2 four-element vectors per thread); shapes: g = 4, P = 8 (6, 8, iters
+// 2) and g = 8, P = 32 (10, 32, iters 1).  ctr is one device word that the
+// call zeroes on `stream` before the launch; late (one device word, not
+// cleared) gains one for every wait that gave up after spin_limit polls.
+// Returns 0, -1 for invalid arguments or a shape without an instance (nothing
+// launched), -4 when a HIP call fails.
+int daso_probe_phased(const void* const* rd32, int32_t r32, const void* const* rd16, int32_t r16, void* const* wr32,
+                      void* const* wr16, uint32_t* ctr, uint32_t* late, int64_t n, int32_t iters, int32_t nwg,
+                      int32_t spin_limit, hipStream_t stream) {
+  if (n <= 0 || n % 4 != 0 || nwg < 1 || nwg > 4096 || spin_limit < 1 || ctr == nullptr || late == nullptr) return -1;
+  if (r32 < 0 || r32 > kMaxRead || r16 < 0 || r16 > kMaxRead || wr32 == nullptr || wr16 == nullptr) return -1;
+  PhasedArgs a = {};
+  for (int i = 0; i < r32; ++i) {
+    if (rd32 == nullptr || rd32[i] == nullptr || (reinterpret_cast<uintptr_t>(rd32[i]) & 15u)) return -1;
+    a.p.rd32[i] = rd32[i];
+  }
+  for (int i = 0; i < r16; ++i) {
+    if (rd16 == nullptr || rd16[i] == nullptr || (reinterpret_cast<uintptr_t>(rd16[i]) & 15u)) return -1;
+    a.p.rd16[i] = rd16[i];
+  }
+  for (int i = 0; i < 2; ++i) {
+    if (wr32[i] == nullptr || (reinterpret_cast<uintptr_t>(wr32[i]) & 15u)) return -1;
+    a.p.wr32[i] = wr32[i];
+  }
+  if (wr16[0] == nullptr || (reinterpret_cast<uintptr_t>(wr16[0]) & 15u)) return -1;
+  a.p.wr16[0] = wr16[0];
+  const void* k = nullptr;
+  int tiles = 0;
+  if (r32 == 6 && r16 == 8 && iters == 2) {
+    k = reinterpret_cast<const void*>(&phased_kernel<6, 8, 2, phased_tiles<2>()>);
+    tiles = phased_tiles<2>();
+  } else if (r32 == 10 && r16 == 32 && iters == 1) {
+    k = reinterpret_cast<const void*>(&phased_kernel<10, 32, 1, phased_tiles<1>()>);
+    tiles = phased_tiles<1>();
+  } else {
+    return -1;
+  }
+  const int64_t tile = int64_t(kProbeBlock) * 4 * iters;
+  const int64_t ntiles = (n + tile - 1) / tile;
+  const int64_t rounds = (ntiles + int64_t(nwg) * tiles - 1) / (int64_t(nwg) * tiles);
+  if (ntiles > INT32_MAX || rounds * 2 * nwg > int64_t(UINT32_MAX)) return -1;
+  a.p.n = n;
+  a.p.ntiles = static_cast<int32_t>(ntiles);
+  a.p.xcd_run = 1;
+  a.ctr = ctr;
+  a.late = late;
+  a.spin_limit = spin_limit;
+  const uint32_t lds = static_cast<uint32_t>(tiles) * iters * kProbeBlock * 16;
+  if (hipMemsetAsync(ctr, 0, sizeof(uint32_t), stream) != hipSuccess) return -4;
+  void* args[] = {&a};
+  return hipLaunchCooperativeKernel(k, dim3(static_cast<uint32_t>(nwg)), dim3(kProbeBlock), args, lds, stream) ==
+                 hipSuccess
+             ? 0
+             : -4;
 }
 
 }  // extern "C"

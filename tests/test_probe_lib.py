@@ -24,6 +24,9 @@ def plib():
     lib.daso_probe_run.argtypes = [ctypes.POINTER(VP), I32, ctypes.POINTER(VP), I32, ctypes.POINTER(VP), I32,
                                    ctypes.POINTER(VP), I32, VP, I64, I32, I32, I32, VP]
     lib.daso_probe_run.restype = ctypes.c_int
+    lib.daso_probe_phased.argtypes = [ctypes.POINTER(VP), I32, ctypes.POINTER(VP), I32, ctypes.POINTER(VP),
+                                      ctypes.POINTER(VP), VP, VP, I64, I32, I32, I32, VP]
+    lib.daso_probe_phased.restype = ctypes.c_int
     return lib
 
 
@@ -76,6 +79,33 @@ def test_probe_rejects_bad_pointers(plib, which, how):
     arr = _ptrs(k, A + 4096 * MB)
     arr[k - 1] = None if how == "null" else A + 4096 * MB + 8
     assert _call(plib, **{which: arr}) == -1
+
+
+def _phased(lib, r32=6, r16=8, n=4096, iters=2, nwg=4, spin=1000, ctr=A + 8192 * MB, late=A + 8193 * MB,
+            rd32=None, rd16=None, wr32=None, wr16=None):
+    rd32 = _ptrs(r32) if rd32 is None else rd32
+    rd16 = _ptrs(r16, A + 1024 * MB) if rd16 is None else rd16
+    wr32 = _ptrs(2, A + 2048 * MB) if wr32 is None else wr32
+    wr16 = _ptrs(1, A + 3072 * MB) if wr16 is None else wr16
+    return lib.daso_probe_phased(rd32, r32, rd16, r16, wr32, wr16, ctr, late, n, iters, nwg, spin, None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(n=0), dict(n=4098), dict(nwg=0), dict(nwg=4097), dict(spin=0), dict(ctr=None), dict(late=None),
+    dict(r32=5), dict(iters=1), dict(r32=10, r16=32, iters=2), dict(r16=16),
+])
+def test_phased_probe_rejects_before_launch(plib, bad):
+    _no_gpu()
+    assert _phased(plib, **bad) == -1
+
+
+@pytest.mark.parametrize("which", ["rd32", "rd16", "wr32", "wr16"])
+def test_phased_probe_rejects_misaligned_pointers(plib, which):
+    _no_gpu()
+    k = {"rd32": 6, "rd16": 8, "wr32": 2, "wr16": 1}[which]
+    arr = _ptrs(k, A + 4096 * MB)
+    arr[k - 1] = A + 4096 * MB + 8
+    assert _phased(plib, **{which: arr}) == -1
 
 
 # ------------------------------------------------------------------ GPU
@@ -175,3 +205,58 @@ def test_probe_writes_exactly_its_elements(plib, case, run, lds):
         assert np.array_equal(got[:n], want16), f"bf16 output differs at {np.flatnonzero(got[:n] != want16)[:5]}"
         assert (got[n:] == SENT16).all(), "bf16 output written past n"
     assert int(sink.abs().sum()) == 0           # the sink is written only on request, never here
+
+
+PHASED_CASES = [  # (r32, r16, iters, n, workgroups): several rounds of staged tiles, ragged tails
+    (6, 8, 2, 4, 1), (6, 8, 2, 2052, 3), (6, 8, 2, 30 * 2048 + 4, 3), (6, 8, 2, 61 * 2048 + 4, 2),
+    (10, 32, 1, 4, 2), (10, 32, 1, 1028, 2), (10, 32, 1, 101 * 1024 + 4, 2),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("spin", [100_000, 1])
+@pytest.mark.parametrize("case", PHASED_CASES, ids=lambda c: "r%d_%d_it%d_n%d_wg%d" % c)
+def test_phased_probe_writes_exactly_its_elements(plib, case, spin):
+    """The chip-wide phased probe writes the bare mix's values to exactly the
+    elements [0, n) of the step's three output streams over several rounds;
+    with a spin limit of one poll its waits give up early (each still ends)
+    and the data is the same."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    r32, r16, iters, n, nwg = case
+    print(f"\n[case] phased probe {case} spin={spin}", flush=True)
+    rng = np.random.default_rng(n * 11 + iters)
+    X32 = [rng.integers(0, 2**32, n + GUARD, dtype=np.uint64).astype(np.uint32) for _ in range(r32)]
+    X16 = [rng.integers(0, 2**16, n + GUARD, dtype=np.uint32).astype(np.uint16) for _ in range(r16)]
+    d32 = [torch.from_numpy(x.view(np.int32)).cuda() for x in X32]
+    d16 = [torch.from_numpy(x.view(np.int16)).cuda() for x in X16]
+    o32 = [torch.full((n + GUARD,), int(SENT32.view(np.int32)), dtype=torch.int32, device="cuda") for _ in range(2)]
+    o16 = [torch.full((n + GUARD,), int(SENT16.view(np.int16)), dtype=torch.int16, device="cuda")]
+    ctr = torch.zeros(4, dtype=torch.int32, device="cuda")
+    late = torch.zeros(4, dtype=torch.int32, device="cuda")
+
+    def arr(ts):
+        a = (VP * max(len(ts), 1))()
+        for k, t in enumerate(ts):
+            a[k] = t.data_ptr()
+        return a
+    torch.cuda.synchronize()
+    rc = plib.daso_probe_phased(arr(d32), r32, arr(d16), r16, arr(o32), arr(o16), VP(ctr.data_ptr()),
+                                VP(late.data_ptr()), n, iters, nwg, spin, VP(torch.cuda.current_stream().cuda_stream))
+    torch.cuda.synchronize()
+    assert rc == 0
+    want32, want16 = _expect(iters, r32, r16, 2, 1, X32, X16, n)
+    for o in o32:
+        got = o.cpu().numpy().view(np.uint32)
+        assert np.array_equal(got[:n], want32), f"fp32 output differs at {np.flatnonzero(got[:n] != want32)[:5]}"
+        assert (got[n:] == SENT32).all(), "fp32 output written past n"
+    got = o16[0].cpu().numpy().view(np.uint16)
+    assert np.array_equal(got[:n], want16), f"bf16 output differs at {np.flatnonzero(got[:n] != want16)[:5]}"
+    assert (got[n:] == SENT16).all(), "bf16 output written past n"
+    tiles = (n + 1024 * iters - 1) // (1024 * iters)
+    per_round = nwg * (72 * 1024 // (iters * 256 * 16))
+    rounds = (tiles + per_round - 1) // per_round
+    assert int(ctr[0]) == 2 * rounds * nwg        # every workgroup met twice per round
+    if spin > 1:
+        assert int(late[0]) == 0
