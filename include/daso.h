@@ -210,8 +210,8 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
 /* For callers that cannot allocate device memory (code under HIP graph capture,
  * tight serving loops, harnesses that forbid hipMalloc): daso_fused_sync_step
  * with the same arguments, results and rules, except that the statistics
- * scratch (24 bytes per tile of 1024 or 2048 parameters plus a 260-byte table,
- * per launch of up to 64 buckets) lives in a fixed array of
+ * scratch (a 256-byte counter, 24 bytes per tile of 1024 or 2048 parameters and
+ * a 260-byte table, per launch of up to 64 buckets) lives in a fixed array of
  * DASO_NOALLOC_SCRATCH_BYTES in device memory instead of an allocated
  * workspace.  The call never allocates or frees memory.  Every GPU the library
  * runs on holds its own copy of that array until the process ends; the first
@@ -221,7 +221,7 @@ int daso_fused_sync_step(const daso_sync_args* args, hipStream_t stream);
  * (host threads may share the stream), but calls on different streams of the
  * same GPU that may run at the same time race on the array and can give wrong
  * statistics; the other outputs are never affected.  A call whose statistics
- * need more than the array holds (more than 699,039 tiles in one launch: at
+ * need more than the array holds (more than 699,029 tiles in one launch: at
  * least about 715 million parameters) returns DASO_ENOSPACE and launches
  * nothing.  Without statistics (stats == NULL) no scratch is used. */
 #define DASO_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)

@@ -23,13 +23,16 @@ using daso::TileBucket;
 using daso::TilePartial;
 
 // ---------------------------------------------------------------- workspace
-// Per (device, stream): the per-tile statistics partials of a fused launch,
-// followed by the launch's table of bucket tile ranges.  Allocated on first use
-// and replaced by one at least twice as large when a larger launch needs it.  A
+// Per (device, stream): the counter of launches that sum their own statistics
+// (kStatsCounterBytes), the per-tile statistics partials of a fused launch and
+// the launch's table of bucket tile ranges.  Allocated on first use and
+// replaced by one at least twice as large when a larger launch needs it.  A
 // replaced buffer is never freed: launches already queued, and graphs captured
 // earlier, may still use it; the doubling keeps the total within twice the
-// largest buffer.  Every launch writes each partial and table entry it later
-// reads, so the contents never need clearing.  A call holds the entry's lock
+// largest buffer.  The counter is zeroed once, by a kernel queued on the
+// stream right after the allocation, and every launch that uses it leaves it
+// at zero; every launch writes each partial and table entry it later reads, so
+// the rest never needs clearing.  A call holds the entry's lock
 // from choosing the buffer until its last launch is queued, so that two host
 // threads sharing a stream cannot queue one call's step between the other
 // call's step and its statistics pass.
@@ -47,12 +50,17 @@ Workspace& workspace_entry(int dev, hipStream_t stream) {
   return g_ws[{dev, stream}];
 }
 
-// With w.mu held: make w hold at least `need` bytes.
-int reserve(Workspace& w, size_t need) {
+// With w.mu held: make w hold at least `need` bytes; a new buffer's counter is
+// zeroed on `stream` before anything else queued there can use it.
+int reserve(Workspace& w, size_t need, hipStream_t stream) {
   if (w.bytes < need) {
     const size_t bytes = std::max<size_t>({need, 2 * w.bytes, size_t(1) << 20});
     void* p = nullptr;
     if (hipMalloc(&p, bytes) != hipSuccess) return DASO_EHIP;
+    if (daso::clear_stats_counter(p, stream) != hipSuccess) {
+      (void)hipFree(p);
+      return DASO_EHIP;
+    }
     w.ptr = p;  // the previous buffer, if any, stays allocated (see above)
     w.bytes = bytes;
   }
@@ -65,11 +73,15 @@ int reserve(Workspace& w, size_t need) {
 // copy until the process ends.  In host code `scratch` names a host-side stand-in,
 // not device memory: the device address is looked up once per device with
 // hipGetSymbolAddress (with that device current) and only that address is
-// handed to kernels.  The kernels write every partial and table entry they read
-// later, so the array never needs clearing.
+// handed to kernels.  Its first kStatsCounterBytes hold the counter of the
+// launches that sum their own statistics: zero when the library is loaded
+// (the array has static storage), and every launch that uses it leaves it at
+// zero.  The kernels write every partial and table entry they read later, so
+// the rest never needs clearing.
 constexpr size_t kScratchBytes = DASO_NOALLOC_SCRATCH_BYTES;
 static_assert(kScratchBytes % 256 == 0, "the scratch size is a whole number of 256-byte blocks");
-static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)];
+static_assert(daso::kStatsCounterBytes % 256 == 0, "the partials start on a 256-byte boundary");
+static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)] = {};
 
 constexpr int kMaxDevices = 64;
 
@@ -336,8 +348,9 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     if (gr.ntiles > INT32_MAX) return DASO_EINVAL;
     max_tiles = std::max(max_tiles, gr.ntiles);
   }
-  // statistics scratch: tile partials, then the table of bucket tile ranges
-  const size_t table_at = static_cast<size_t>(max_tiles) * sizeof(TilePartial);
+  // statistics scratch: the counter, the tile partials, then the table of bucket tile ranges
+  const size_t partials_at = daso::kStatsCounterBytes;
+  const size_t table_at = partials_at + static_cast<size_t>(max_tiles) * sizeof(TilePartial);
   const size_t need = table_at + (daso::kLaunchBuckets + 1) * sizeof(int32_t);
   if (with_stats && space == Space::kFixed && need > kScratchBytes) return DASO_ENOSPACE;
   int dev = 0;
@@ -346,6 +359,7 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
   const int streams = launch_streams(mode, a);
   const int32_t lds = lds_of(mode, streams);
   std::unique_lock<std::mutex> hold;
+  uint32_t* counter = nullptr;
   if (with_stats) {
     void* base = nullptr;
     if (space == Space::kFixed) {
@@ -357,11 +371,12 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     } else {
       Workspace& w = workspace_entry(dev, stream);
       hold = std::unique_lock<std::mutex>(w.mu);
-      const int rc = reserve(w, need);
+      const int rc = reserve(w, need, stream);
       if (rc != DASO_OK) return rc;
       base = w.ptr;
     }
-    a.partials = static_cast<TilePartial*>(base);
+    counter = static_cast<uint32_t*>(base);
+    a.partials = reinterpret_cast<TilePartial*>(static_cast<char*>(base) + partials_at);
     a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(base) + table_at);
   }
   // the tile order of a single fused launch may be chosen per shape (above)
@@ -371,6 +386,8 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     const Group gr = group_at(b, nb, i, tile);
     fill_group(a, b, gr, tile);
     a.stats = with_stats ? stats + gr.first : nullptr;
+    // a launch of few tiles sums its own statistics in its last workgroup
+    a.done = (with_stats && a.ntiles <= daso::kFinishStatsMaxTiles) ? counter : nullptr;
     const int32_t rule = xcd_run_of(mode, streams, a.ntiles, tile);
     a.xcd_run = rule;
     Tune* t = nullptr;

@@ -455,6 +455,65 @@ __device__ __forceinline__ void run_tile(const StepArgs& a, int64_t abase, int64
   }
 }
 
+// The statistics of one bucket: the whole workgroup sums the tile partials
+// [t0, t1) in a fixed assignment and reduction tree (thread k adds partials
+// t0 + k, t0 + k + kBlock, ... in that order), so the result does not depend on
+// timing, on which kernel runs it or on kLoads.  Valid in thread 0.
+// The sum is latency-bound: each thread issues the loads of up to kLoads
+// partials before it adds them in tile order.  Missing ones count as zeros,
+// which leaves every sum unchanged (sums of squares are never -0).
+template <int kLoads>
+__device__ __forceinline__ Acc64 bucket_stats(const TilePartial* partials, int t0, int t1) {
+  Acc64 v = {0.0, 0.0, 0};
+  for (int base = t0 + static_cast<int>(threadIdx.x); base < t1; base += kBlock * kLoads) {
+    TilePartial p[kLoads];
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) {
+      const int j = base + u * kBlock;
+      p[u] = j < t1 ? partials[j] : TilePartial{0.0, 0.0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) {
+      v.gsq += p[u].grad_sq;
+      v.dsq += p[u].delta_sq;
+      v.nf += p[u].nonfinite;
+    }
+  }
+  return block_sum(v);
+}
+
+__device__ __forceinline__ void put_stats(daso_bucket_stats* out, const Acc64& r) {
+  out->grad_sq = r.gsq;
+  out->delta_sq = r.dsq;
+  out->nonfinite = r.nf;
+}
+
+// A launch of few tiles sums its statistics in its own last workgroup instead
+// of a second launch.  Each workgroup makes its partials visible to the whole
+// chip (an agent-scope release fence: the XCD's L2 writes them back) and then
+// counts itself done; the one that counts last takes an acquire fence and sums
+// every bucket with the same code and order as stats_kernel, so the results
+// are the same bits, and sets the counter back to zero for the next launch.
+// The fences cost about 0.1 us per workgroup, which is why only small launches
+// (at most kFinishStatsMaxTiles tiles, one workgroup each) take this path.
+__device__ __forceinline__ void finish_stats_if_last(const StepArgs& a) {
+  __shared__ bool last;
+  __syncthreads();  // thread 0 has written this workgroup's partials
+  if (threadIdx.x == 0) {
+    __threadfence();
+    last = atomicAdd(a.done, 1u) == gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  for (int i = 0; i < a.nb; ++i) {
+    const int t1 = i + 1 < a.nb ? a.b[i + 1].first_tile : a.ntiles;
+    const Acc64 r = bucket_stats<1>(a.partials, a.b[i].first_tile, t1);  // at most one partial per thread
+    if (threadIdx.x == 0) put_stats(a.stats + i, r);
+  }
+  if (threadIdx.x == 0) atomicExch(a.done, 0u);
+}
+
 // ------------------------------------------------------------------- kernel
 // One workgroup per tile; the loop serves a grid smaller than the tiles (the
 // host caps the grid for launches of more than 2^20 tiles).
@@ -498,43 +557,25 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
       }
     }
   }
+  if constexpr (STATS && MODE == kModeFused) {
+    if (a.done != nullptr) finish_stats_if_last(a);
+  }
 }
 
-// Statistics of one launch: workgroup i sums the tile partials of bucket i in
-// tile order (a fixed assignment and reduction tree, so the result does not
-// depend on timing).  Runs after step_kernel on the same stream, which makes
-// every partial, and the tile table, visible without any fence inside
-// step_kernel.
+// Sets the counter of StepArgs::done at the start of a new statistics buffer
+// to zero (a kernel rather than a memset, so that it may also sit in a graph).
+__global__ void clear_counter_kernel(uint32_t* counter) {
+  if (threadIdx.x == 0) *counter = 0u;
+}
+
+// Statistics of one launch: workgroup i sums the tile partials of bucket i.
+// Runs after step_kernel on the same stream, which makes every partial, and the
+// tile table, visible without any fence inside step_kernel.
 __global__ __launch_bounds__(kBlock) void stats_kernel(const StatsArgs a) {
   const int i = static_cast<int>(blockIdx.x);
-  const int t0 = a.tile_table[i];
-  const int t1 = a.tile_table[i + 1];
-  Acc64 v = {0.0, 0.0, 0};
-  // The kernel is latency-bound: each thread issues the loads of up to 16
-  // partials (about 12 for a 25 MiB bucket of 2048-element tiles) before it
-  // adds them in tile order.  Missing ones count as zeros, which leaves every
-  // sum unchanged (sums of squares are never -0).
-  constexpr int kLoads = 16;
-  for (int base = t0 + static_cast<int>(threadIdx.x); base < t1; base += kBlock * kLoads) {
-    TilePartial p[kLoads];
-#pragma unroll
-    for (int u = 0; u < kLoads; ++u) {
-      const int j = base + u * kBlock;
-      p[u] = j < t1 ? a.partials[j] : TilePartial{0.0, 0.0, 0};
-    }
-#pragma unroll
-    for (int u = 0; u < kLoads; ++u) {
-      v.gsq += p[u].grad_sq;
-      v.dsq += p[u].delta_sq;
-      v.nf += p[u].nonfinite;
-    }
-  }
-  const Acc64 r = block_sum(v);
-  if (threadIdx.x == 0) {
-    a.stats[i].grad_sq = r.gsq;
-    a.stats[i].delta_sq = r.dsq;
-    a.stats[i].nonfinite = r.nf;
-  }
+  // 16 loads per thread in flight: about 12 partials each for a 25 MiB bucket of 2048-element tiles
+  const Acc64 r = bucket_stats<16>(a.partials, a.tile_table[i], a.tile_table[i + 1]);
+  if (threadIdx.x == 0) put_stats(a.stats + i, r);
 }
 
 // Fused instances with compile-time stream counts for the node shapes: g = 4
@@ -658,7 +699,7 @@ struct Launcher {
     void* args[] = {const_cast<StepArgs*>(&a)};
     const hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&step_kernel<MODE, G, PP, STATS, XF>),
                                          dim3(grid), dim3(kBlock), args, lds, stream);
-    if (e != hipSuccess || !STATS) return e;
+    if (e != hipSuccess || !STATS || a.done != nullptr) return e;
     StatsArgs sa = {a.partials, a.tile_table, a.stats, a.nb};
     void* sargs[] = {&sa};
     return hipLaunchKernel(reinterpret_cast<const void*>(&stats_kernel), dim3(a.nb), dim3(kBlock), sargs, 0, stream);
@@ -681,6 +722,11 @@ int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& a) {
 hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& a, uint32_t grid, uint32_t lds,
                        hipStream_t stream) {
   return dispatch(mode, with_stats, a, Launcher{a, grid, lds, stream});
+}
+
+hipError_t clear_stats_counter(void* buffer, hipStream_t stream) {
+  void* args[] = {&buffer};
+  return hipLaunchKernel(reinterpret_cast<const void*>(&clear_counter_kernel), dim3(1), dim3(64), args, 0, stream);
 }
 
 }  // namespace daso

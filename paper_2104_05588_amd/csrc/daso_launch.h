@@ -70,6 +70,17 @@ constexpr int32_t kCuLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 // covers the kernel's own few bytes of LDS and the allocation granule.
 inline int32_t lds_for_workgroups_per_cu(int32_t k) { return k >= 1 ? kCuLdsBytes / k - 1024 : 0; }
 
+// A fused launch with statistics of at most this many tiles has its last
+// workgroup sum the statistics (StepArgs::done) instead of a second launch:
+// each of its workgroups pays an agent-scope fence, which is cheaper than a
+// launch for a few dozen workgroups and far dearer for thousands.
+constexpr int64_t kFinishStatsMaxTiles = 64;
+
+// Bytes at the start of a statistics scratch buffer that hold the counter of
+// StepArgs::done (zero whenever no launch is running); the tile partials and
+// the bucket table follow.
+constexpr size_t kStatsCounterBytes = 256;
+
 enum Mode : int { kModeAvg = 0, kModePack = 1, kModeMerge = 2, kModeFused = 3 };
 
 struct TileBucket {
@@ -99,6 +110,9 @@ struct StepArgs {
   int32_t* tile_table;   // (stats only) nb + 1 entries written by workgroup 0 for stats_kernel:
                          // the first tile of each bucket, then ntiles
   daso_bucket_stats* stats;  // per-bucket outputs (stats only), already offset to this launch
+  uint32_t* done;        // (stats only) nonnull: no stats_kernel; the workgroup that finishes last
+                         // sums the statistics.  A counter that is zero before the launch and
+                         // that the launch leaves at zero.
   int32_t g;
   int32_t P;
   float lr;
@@ -151,5 +165,8 @@ int64_t tile_elems(Mode mode, bool with_stats, const StepArgs& args);
 // then looping over tiles grid apart), each holding `lds` bytes of LDS.
 hipError_t launch_step(Mode mode, bool with_stats, const StepArgs& args, uint32_t grid, uint32_t lds,
                        hipStream_t stream);
+
+// Enqueue the zeroing of the counter at the start of a new statistics buffer.
+hipError_t clear_stats_counter(void* buffer, hipStream_t stream);
 
 }  // namespace daso

@@ -202,16 +202,16 @@ def test_fused_rejects(lib, entry):
 
 
 def test_noalloc_rejects_statistics_beyond_its_scratch(lib):
-    """daso_fused_sync_step_noalloc keeps the statistics partials (24 bytes per
-    tile) and the 65-entry table of a launch in its fixed 16 MiB array: 699,039
-    tiles fit, one more is DASO_ENOSPACE before any HIP call.  g = 1, P = 0 runs
+    """daso_fused_sync_step_noalloc keeps a 256-byte counter, the statistics
+    partials (24 bytes per tile) and the 65-entry table of a launch in its fixed
+    16 MiB array: 699,029 tiles fit, one more is DASO_ENOSPACE before any HIP call.  g = 1, P = 0 runs
     2048-element tiles.  Without statistics there is no limit; with room the
     call goes on to HIP, which fails here without a GPU."""
     _no_gpu()
     f = lib.daso_fused_sync_step_noalloc
     GB8 = 8 << 30
     assert L.DASO_ENOSPACE == -5 and "DASO_ENOSPACE" in L.status_string(L.DASO_ENOSPACE)
-    fit = 699_039
+    fit = 699_029
 
     def rc(n, stats=True, nb=1):
         a = L.daso_sync_args()
@@ -224,7 +224,7 @@ def test_noalloc_rejects_statistics_beyond_its_scratch(lib):
         a.lr, a.mu = 0.1, 0.9
         return f(ctypes.byref(a), None)
 
-    assert (24 * fit + 65 * 4) <= (16 << 20) < 24 * (fit + 1) + 65 * 4
+    assert (256 + 24 * fit + 65 * 4) <= (16 << 20) < 256 + 24 * (fit + 1) + 65 * 4
     assert rc(fit * 2048 + 1) == L.DASO_ENOSPACE
     assert rc(fit * 2048 + 1, nb=2) == L.DASO_ENOSPACE
     assert rc(fit * 2048) == L.DASO_EHIP

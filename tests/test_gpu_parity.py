@@ -690,12 +690,15 @@ def test_fused_beyond_int32_element_count():
     assert got[0][2] == 0 and got[1][2] == 0 and got[0][0] > 0 and got[1][1] > 0
 
 
-def test_fused_step_replays_in_a_hip_graph():
+@pytest.mark.parametrize("n", [300_001, 60_001], ids=["statistics_pass", "last_workgroup_sums"])
+def test_fused_step_replays_in_a_hip_graph(n):
     """After a first eager call (which allocates the statistics workspace), the
     fused step can be captured in a graph: every replay, with eager work and
-    synchronisations between replays, gives the eager result bit for bit."""
+    synchronisations between replays, gives the eager result bit for bit.  The
+    larger launch sums its statistics in a second kernel; the smaller one (at
+    most 64 tiles) in its last workgroup, whose counter every replay must leave
+    at zero."""
     rng = np.random.default_rng(77)
-    n = 300_001
     bks = random_buckets(rng, n, 3)
     inp = random_inputs(rng, n, 4, 8)
     announce("fused step in a HIP graph")
@@ -800,6 +803,22 @@ def test_earlier_hip_error_is_neither_blamed_nor_consumed():
     got = {"params": host_f32(x), "momentum": host_f32(m), "wire": host_u16(wire), "grad_avg": None,
            "stats": daso.decode_stats(st)}
     compare_fused(got, want, "after a failed hipMalloc")
+
+
+def test_small_and_large_launches_alternate_on_one_stream():
+    """Launches of at most 64 tiles sum their statistics in their last workgroup
+    (a counter in the workspace that each leaves at zero), larger ones in a
+    second kernel; mixed on one stream, every call's statistics and outputs
+    match the oracle."""
+    rng = np.random.default_rng(515)
+    sizes = [20_000, 130_000, 65_536, 1, 400_000, 131_072, 2_000_003, 9_000]
+    for k, n in enumerate(sizes):
+        bks = random_buckets(rng, n, int(rng.integers(1, 5)))
+        inp = random_inputs(rng, n, 4, 8)
+        announce("alternating launch sizes, call", k, "n =", n)
+        got = run_fused(inp, bks)
+        want = O.fused_sync_step(inp["grads"], inp["params"], inp["momentum"], inp["stale"], bks, 0.1, 0.9)
+        compare_fused(got, want, f"alternating launch sizes, call {k} (n = {n})")
 
 
 def test_tile_order_choice_keeps_results_and_a_pending_error():
