@@ -70,10 +70,12 @@ constexpr int32_t kCuLdsBytes = 160 * 1024;  // LDS per CU on gfx950
 // covers the kernel's own few bytes of LDS and the allocation granule.
 inline int32_t lds_for_workgroups_per_cu(int32_t k) { return k >= 1 ? kCuLdsBytes / k - 1024 : 0; }
 
-// A fused launch with statistics of at most this many tiles has its last
-// workgroup sum the statistics (StepArgs::done) instead of a second launch:
-// each of its workgroups pays an agent-scope fence, which is cheaper than a
-// launch for a few dozen workgroups and far dearer for thousands.
+// An eager fused launch with statistics of at most this many tiles has its
+// last workgroup sum the statistics (StepArgs::done) instead of a second
+// launch: each of its workgroups pays an agent-scope fence (about 0.1 us of GPU
+// time each), which is cheaper than a launch's host cost for a few dozen
+// workgroups and far dearer for thousands.  Captured calls keep the second
+// launch, whose host cost a graph replay does not pay.
 constexpr int64_t kFinishStatsMaxTiles = 64;
 
 // Bytes at the start of a statistics scratch buffer that hold the counter of

@@ -690,14 +690,13 @@ def test_fused_beyond_int32_element_count():
     assert got[0][2] == 0 and got[1][2] == 0 and got[0][0] > 0 and got[1][1] > 0
 
 
-@pytest.mark.parametrize("n", [300_001, 60_001], ids=["statistics_pass", "last_workgroup_sums"])
+@pytest.mark.parametrize("n", [300_001, 60_001], ids=["large_launch", "small_launch"])
 def test_fused_step_replays_in_a_hip_graph(n):
     """After a first eager call (which allocates the statistics workspace), the
     fused step can be captured in a graph: every replay, with eager work and
     synchronisations between replays, gives the eager result bit for bit.  The
-    larger launch sums its statistics in a second kernel; the smaller one (at
-    most 64 tiles) in its last workgroup, whose counter every replay must leave
-    at zero."""
+    eager call of the small launch (at most 64 tiles) sums its statistics in its
+    last workgroup, the captured one in the statistics kernel: the same bits."""
     rng = np.random.default_rng(77)
     bks = random_buckets(rng, n, 3)
     inp = random_inputs(rng, n, 4, 8)
