@@ -56,7 +56,10 @@
  *  - On an argument error (DASO_EINVAL, DASO_EALIGN, DASO_EALIAS) nothing is
  *    launched and the buffers are untouched; daso_status_string names the
  *    status.  A call may queue more than one kernel: one per 64 buckets of its
- *    table, and a statistics pass after each fused launch with statistics.  If
+ *    table, and a statistics pass after each fused launch with statistics
+ *    (except an eager launch of at most 64 tiles, whose last workgroup sums
+ *    its statistics itself; a call being captured into a graph keeps the
+ *    pass), and one zeroing kernel when a statistics workspace is new.  If
  *    queueing one of them fails (DASO_EHIP), the kernels queued before it still
  *    run: the outputs (params, momentum, wire, grad_avg, stats) of the buckets
  *    they cover may then already be updated, the others are untouched.
