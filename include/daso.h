@@ -57,9 +57,10 @@
  *    launched and the buffers are untouched; daso_status_string names the
  *    status.  A call may queue more than one kernel: one per 64 buckets of its
  *    table, and a statistics pass after each fused launch with statistics
- *    (except an eager launch of at most 64 tiles, whose last workgroup sums
- *    its statistics itself; a call being captured into a graph keeps the
- *    pass), and one zeroing kernel when a statistics workspace is new.  If
+ *    (except an eager launch of at most 64 tiles of daso_fused_sync_step,
+ *    whose last workgroup sums its statistics itself; a call being captured
+ *    into a graph keeps the pass, as daso_fused_sync_step_noalloc always
+ *    does), and one zeroing kernel when a statistics workspace is new.  If
  *    queueing one of them fails (DASO_EHIP), the kernels queued before it still
  *    run: the outputs (params, momentum, wire, grad_avg, stats) of the buckets
  *    they cover may then already be updated, the others are untouched.

@@ -73,15 +73,14 @@ int reserve(Workspace& w, size_t need, hipStream_t stream) {
 // copy until the process ends.  In host code `scratch` names a host-side stand-in,
 // not device memory: the device address is looked up once per device with
 // hipGetSymbolAddress (with that device current) and only that address is
-// handed to kernels.  Its first kStatsCounterBytes hold the counter of the
-// launches that sum their own statistics: zero when the library is loaded
-// (the array has static storage), and every launch that uses it leaves it at
-// zero.  The kernels write every partial and table entry they read later, so
-// the rest never needs clearing.
+// handed to kernels.  It has the workspace's layout, but its first
+// kStatsCounterBytes are never used: calls through it keep the statistics
+// kernel (see run_groups).  The kernels write every partial and table entry
+// they read later, so the array never needs clearing.
 constexpr size_t kScratchBytes = DASO_NOALLOC_SCRATCH_BYTES;
 static_assert(kScratchBytes % 256 == 0, "the scratch size is a whole number of 256-byte blocks");
 static_assert(daso::kStatsCounterBytes % 256 == 0, "the partials start on a 256-byte boundary");
-static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)] = {};
+static __device__ __align__(256) uint64_t scratch[kScratchBytes / sizeof(uint64_t)];
 
 constexpr int kMaxDevices = 64;
 
@@ -392,8 +391,13 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     // an eager launch of few tiles sums its own statistics in its last
     // workgroup: that saves a launch's host cost (about 2.6 us) for fences that
     // cost the GPU about 0.1 us per workgroup; a graph replays launches without
-    // that host cost, so a captured call keeps the statistics kernel
-    a.done = (with_stats && a.ntiles <= daso::kFinishStatsMaxTiles && !capturing) ? counter : nullptr;
+    // that host cost, so a captured call keeps the statistics kernel, and so
+    // does the no-alloc entry point, whose scratch every call on the GPU shares:
+    // two of its calls racing on another stream could leave the counter wrong
+    // for later calls, not only their own statistics
+    a.done = (with_stats && a.ntiles <= daso::kFinishStatsMaxTiles && !capturing && space == Space::kAllocated)
+                 ? counter
+                 : nullptr;
     const int32_t rule = xcd_run_of(mode, streams, a.ntiles, tile);
     a.xcd_run = rule;
     Tune* t = nullptr;
