@@ -60,7 +60,8 @@
  *    (except an eager launch of at most 64 tiles of daso_fused_sync_step,
  *    whose last workgroup sums its statistics itself; a call being captured
  *    into a graph keeps the pass, as daso_fused_sync_step_noalloc always
- *    does), and one zeroing kernel when a statistics workspace is new.  If
+ *    does), and one zeroing kernel on the first eager call that uses a new
+ *    statistics workspace.  If
  *    queueing one of them fails (DASO_EHIP), the kernels queued before it still
  *    run: the outputs (params, momentum, wire, grad_avg, stats) of the buckets
  *    they cover may then already be updated, the others are untouched.

@@ -29,10 +29,11 @@ using daso::TilePartial;
 // replaced by one at least twice as large when a larger launch needs it.  A
 // replaced buffer is never freed: launches already queued, and graphs captured
 // earlier, may still use it; the doubling keeps the total within twice the
-// largest buffer.  The counter is zeroed once, by a kernel queued on the
-// stream right after the allocation, and every launch that uses it leaves it
-// at zero; every launch writes each partial and table entry it later reads, so
-// the rest never needs clearing.  A call holds the entry's lock
+// largest buffer.  The counter is zeroed once, by a kernel that the first
+// eager (not captured) call needing it queues on the stream, and every launch
+// that uses it leaves it at zero; every launch writes each partial and table
+// entry it later reads, so the rest never needs clearing.  A call holds the
+// entry's lock
 // from choosing the buffer until its last launch is queued, so that two host
 // threads sharing a stream cannot queue one call's step between the other
 // call's step and its statistics pass.
@@ -40,6 +41,7 @@ struct Workspace {
   std::mutex mu;
   void* ptr = nullptr;
   size_t bytes = 0;
+  bool counter_zeroed = false;  // the zeroing of ptr's counter is queued on the stream
 };
 
 std::mutex g_ws_mu;  // guards the map itself; nodes never move or go away
@@ -50,20 +52,25 @@ Workspace& workspace_entry(int dev, hipStream_t stream) {
   return g_ws[{dev, stream}];
 }
 
-// With w.mu held: make w hold at least `need` bytes; a new buffer's counter is
-// zeroed on `stream` before anything else queued there can use it.
-int reserve(Workspace& w, size_t need, hipStream_t stream) {
+// With w.mu held: make w hold at least `need` bytes.
+int reserve(Workspace& w, size_t need) {
   if (w.bytes < need) {
     const size_t bytes = std::max<size_t>({need, 2 * w.bytes, size_t(1) << 20});
     void* p = nullptr;
     if (hipMalloc(&p, bytes) != hipSuccess) return DASO_EHIP;
-    if (daso::clear_stats_counter(p, stream) != hipSuccess) {
-      (void)hipFree(p);
-      return DASO_EHIP;
-    }
     w.ptr = p;  // the previous buffer, if any, stays allocated (see above)
     w.bytes = bytes;
+    w.counter_zeroed = false;
   }
+  return DASO_OK;
+}
+
+// With w.mu held, from an eager call: queue the zeroing of w's counter on
+// `stream` once per buffer, before any launch that uses it.
+int zero_counter_once(Workspace& w, hipStream_t stream) {
+  if (w.counter_zeroed) return DASO_OK;
+  if (daso::clear_stats_counter(w.ptr, stream) != hipSuccess) return DASO_EHIP;
+  w.counter_zeroed = true;
   return DASO_OK;
 }
 
@@ -373,11 +380,16 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     } else {
       Workspace& w = workspace_entry(dev, stream);
       hold = std::unique_lock<std::mutex>(w.mu);
-      const int rc = reserve(w, need, stream);
+      const int rc = reserve(w, need);
       if (rc != DASO_OK) return rc;
       base = w.ptr;
+      // the last-workgroup statistics of small eager launches count in w's counter
+      if (!capturing) {
+        const int zc = zero_counter_once(w, stream);
+        if (zc != DASO_OK) return zc;
+        counter = static_cast<uint32_t*>(base);
+      }
     }
-    counter = static_cast<uint32_t*>(base);
     a.partials = reinterpret_cast<TilePartial*>(static_cast<char*>(base) + partials_at);
     a.tile_table = reinterpret_cast<int32_t*>(static_cast<char*>(base) + table_at);
   }
@@ -391,13 +403,11 @@ int run_groups(daso::Mode mode, StepArgs& a, const daso_bucket* b, int32_t nb,
     // an eager launch of few tiles sums its own statistics in its last
     // workgroup: that saves a launch's host cost (about 2.6 us) for fences that
     // cost the GPU about 0.1 us per workgroup; a graph replays launches without
-    // that host cost, so a captured call keeps the statistics kernel, and so
-    // does the no-alloc entry point, whose scratch every call on the GPU shares:
-    // two of its calls racing on another stream could leave the counter wrong
-    // for later calls, not only their own statistics
-    a.done = (with_stats && a.ntiles <= daso::kFinishStatsMaxTiles && !capturing && space == Space::kAllocated)
-                 ? counter
-                 : nullptr;
+    // that host cost, so a captured call keeps the statistics kernel (counter
+    // stays null), and so does the no-alloc entry point, whose scratch every
+    // call on the GPU shares: two of its calls racing on another stream could
+    // leave a counter wrong for later calls, not only their own statistics
+    a.done = (counter != nullptr && a.ntiles <= daso::kFinishStatsMaxTiles) ? counter : nullptr;
     const int32_t rule = xcd_run_of(mode, streams, a.ntiles, tile);
     a.xcd_run = rule;
     Tune* t = nullptr;
